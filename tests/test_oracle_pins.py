@@ -1,0 +1,328 @@
+"""Pins for the CPU oracle: each test ties it to something other than itself.
+
+Kinds of pin used (RouteBalance, arXiv 2606.17949):
+  * hand-worked examples with their arithmetic written out (tests/golden/);
+  * an independent brute force (numpy full distance matrix + lexsort) on tiny banks;
+  * closed forms (constant labels, k = N, k = 1, the inter-batch drain);
+  * invariants of Eq. 1 and of the greedy loop of Alg. 1 (simplex corners,
+    scale invariance, score range, conservation of the dead-reckoned state,
+    w_lat = 0 reducing the greedy to a row-wise argmax).
+The paper prints no worked example of its own, so no pin is a printed paper value.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _gold(name):
+    with open(os.path.join(GOLD, name)) as f:
+        return json.load(f)
+
+
+def _inst_from(g):
+    return synth.Instances(np.array(g["model"], np.int32), np.array(g["prefill_q"], np.float32),
+                           np.array(g["decode_q"], np.float32),
+                           np.array(g["prefill_rate"], np.float32),
+                           np.array(g["decode_rate"], np.float32),
+                           np.array(g["price_in"], np.float32), np.array(g["price_out"], np.float32))
+
+
+# ----------------------------------------------------------------------------- KNN
+
+
+def test_knn_hand_example_with_ties():
+    g = _gold("knn_ties_d2.json")
+    q = np.array(g["query"], np.float32)
+    x = np.array(g["bank"], np.float32)
+    idx, dist = oracle.knn(q, x, g["k"])
+    assert idx.tolist() == g["expect_idx"]
+    np.testing.assert_allclose(dist, g["expect_dist"], rtol=0, atol=1e-6)
+    idx, dist = oracle.knn(q, x, x.shape[0])
+    assert idx.tolist() == g["full_order_idx"]
+    np.testing.assert_allclose(dist, g["full_order_dist"], rtol=0, atol=1e-6)
+
+
+def _brute(q64, x64, k):
+    """Independent brute force: full fp64 distance matrix, lexsort by (dist, idx)."""
+    out_i, out_d = [], []
+    for b in range(q64.shape[0]):
+        dd = ((x64 - q64[b][None, :]) ** 2).sum(axis=1)
+        order = np.lexsort((np.arange(x64.shape[0]), dd))[:k]
+        out_i.append(order)
+        out_d.append(dd[order])
+    return np.array(out_i, np.int32), np.array(out_d)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("N,d,k", [(10, 3, 10), (257, 8, 1), (1000, 16, 10), (4096, 64, 17),
+                                   (333, 40, 64)])
+def test_knn_matches_bruteforce(dtype, N, d, k):
+    rng = np.random.default_rng(N * 7 + d)
+    B = 5
+    q = torch.from_numpy(rng.standard_normal((B, d)).astype(np.float32))
+    x = torch.from_numpy(rng.standard_normal((N, d)).astype(np.float32))
+    if dtype == "bf16":
+        q, x = q.bfloat16(), x.bfloat16()
+    # plant exact duplicates and exact distance ties
+    x[N // 2] = x[N // 3]
+    x[N - 1] = q[0]
+    idx, dist = oracle.knn(q, x, k)
+    ei, ed = _brute(q.double().numpy(), x.double().numpy(), k)
+    assert np.array_equal(idx, ei)
+    np.testing.assert_allclose(dist, ed, rtol=1e-12, atol=1e-12)
+
+
+def test_knn_special_cases():
+    rng = np.random.default_rng(3)
+    x = rng.standard_normal((50, 6)).astype(np.float32)
+    q = x[[7, 20]].copy()
+    # k = 1 returns the row itself at distance 0
+    idx, dist = oracle.knn(q, x, 1)
+    assert idx[:, 0].tolist() == [7, 20] and np.all(dist == 0)
+    # a duplicated row: both copies at distance 0, lower index first
+    x2 = np.concatenate([x, x[[7]]])
+    idx, dist = oracle.knn(q[:1], x2, 2)
+    assert idx[0].tolist() == [7, 50] and np.all(dist[0] == 0)
+    # k = N gives every row, ascending
+    idx, dist = oracle.knn(q, x, 50)
+    assert sorted(idx[0].tolist()) == list(range(50))
+    assert np.all(np.diff(dist, axis=1) >= 0)
+    # all rows equal: the order is plain index order
+    x3 = np.ones((9, 4), np.float32)
+    idx, _ = oracle.knn(np.zeros((1, 4), np.float32), x3, 9)
+    assert idx[0].tolist() == list(range(9))
+
+
+def test_knn_rejects_bad_args():
+    x = np.zeros((4, 2), np.float32)
+    with pytest.raises(ValueError):
+        oracle.knn(x[:1], x, 5)            # k > N
+    with pytest.raises(ValueError):
+        oracle.knn(x[:1], x, 0)
+
+
+# ----------------------------------------------------------------------------- predict
+
+
+def test_predict_hand_example():
+    g = _gold("knn_ties_d2.json")
+    idx, _ = oracle.knn(np.array(g["query"], np.float32), np.array(g["bank"], np.float32), g["k"])
+    qh, lh = oracle.predict(idx, np.array(g["qual"], np.float32), np.array(g["len"], np.float32))
+    np.testing.assert_allclose(qh, g["expect_q_hat"], rtol=1e-7)
+    np.testing.assert_allclose(lh, g["expect_l_hat"], rtol=1e-12)
+
+
+def test_predict_closed_forms():
+    rng = np.random.default_rng(5)
+    N, M, d = 40, 3, 5
+    x = rng.standard_normal((N, d)).astype(np.float32)
+    q = rng.standard_normal((4, d)).astype(np.float32)
+    qual = rng.uniform(0, 1, (N, M)).astype(np.float32)
+    ln = rng.integers(1, 500, (N, M)).astype(np.float32)
+    # constant labels give that constant
+    idx, _ = oracle.knn(q, x, 7)
+    qh, lh = oracle.predict(idx, np.full((N, M), 0.25, np.float32), np.full((N, M), 42, np.float32))
+    assert np.all(qh == 0.25) and np.all(lh == 42)
+    # k = N gives the global mean per model
+    idx, _ = oracle.knn(q, x, N)
+    qh, lh = oracle.predict(idx, qual, ln)
+    np.testing.assert_allclose(qh, np.broadcast_to(qual.astype(np.float64).mean(0), qh.shape),
+                               rtol=1e-12)
+    np.testing.assert_allclose(lh, np.broadcast_to(ln.astype(np.float64).mean(0), lh.shape),
+                               rtol=1e-12)
+    # k = 1 gives the nearest row's labels exactly, per model column
+    idx, _ = oracle.knn(q, x, 1)
+    qh, lh = oracle.predict(idx, qual, ln)
+    assert np.array_equal(qh, qual[idx[:, 0]].astype(np.float64))
+    assert np.array_equal(lh, ln[idx[:, 0]].astype(np.float64))
+
+
+# ----------------------------------------------------------------------------- score
+
+
+def test_score_hand_example():
+    g = _gold("score_2x3.json")
+    inst = _inst_from(g)
+    S0 = oracle.score(g["q_hat"], g["l_hat"], g["prompt_len"], inst, g["weights"])
+    np.testing.assert_allclose(S0, g["expect_S0"], rtol=1e-12)
+    for r in range(2):
+        S, T, C = oracle.score_row(g["q_hat"][r], g["l_hat"][r], g["prompt_len"][r], inst,
+                                   inst.prefill_q, inst.decode_q, g["weights"])
+        np.testing.assert_allclose(T, g["expect_T0"][r], rtol=1e-12)
+        np.testing.assert_allclose(C, g["expect_C"][r], rtol=1e-6)   # fp32 prices
+        np.testing.assert_allclose(S, g["expect_S0"][r], rtol=1e-12)
+
+
+def test_assign_hand_example_and_corners():
+    g = _gold("score_2x3.json")
+    inst = _inst_from(g)
+    res = oracle.assign(g["q_hat"], g["l_hat"], g["prompt_len"], inst, g["weights"], trace=True)
+    assert res["assign"].tolist() == g["expect_assign"]
+    np.testing.assert_allclose(res["chosen"], g["expect_chosen"], rtol=1e-12)
+    np.testing.assert_array_equal(res["p"], g["expect_final_p"])
+    np.testing.assert_array_equal(res["a"], g["expect_final_a"])
+    # step 1 is scored after step 0's update
+    S, _, _ = oracle.score_row(g["q_hat"][1], g["l_hat"][1], g["prompt_len"][1], inst,
+                               res["trace_p"][1], res["trace_a"][1], g["weights"])
+    np.testing.assert_allclose(S, g["expect_step1_S"], rtol=1e-12)
+    for c in g["corners"]:
+        r = oracle.assign(g["q_hat"], g["l_hat"], g["prompt_len"], inst, c["weights"])
+        assert r["assign"].tolist() == c["assign"], c
+        np.testing.assert_array_equal(r["p"], c["final_p"])
+        np.testing.assert_array_equal(r["a"], c["final_a"])
+
+
+def test_cost_uses_input_price_for_prompt_and_output_price_for_output():
+    # i0 charges only input tokens, i1 only output tokens. A short prompt with a
+    # long predicted output is cheap on i0; a long prompt with a short output is
+    # cheap on i1. Swapping the two prices in Eq. 2 flips both picks.
+    inst = synth.Instances(np.array([0, 0], np.int32), np.zeros(2, np.float32),
+                           np.zeros(2, np.float32), np.full(2, 1000, np.float32),
+                           np.full(2, 100, np.float32), np.array([1e-3, 0], np.float32),
+                           np.array([0, 1e-3], np.float32))
+    qh = [[0.5], [0.5]]
+    lh = [[1000.0], [10.0]]
+    res = oracle.assign(qh, lh, [10, 1000], inst, (0, 0, 1))
+    assert res["assign"].tolist() == [0, 1]
+
+
+def test_latency_uses_prefill_rate_for_prompt_and_decode_rate_for_output():
+    # i0 prefills fast but decodes slowly; i1 the reverse. Both idle. A long
+    # prompt with a 1-token output is faster on i0; a short prompt with a long
+    # output is faster on i1.
+    inst = synth.Instances(np.array([0, 0], np.int32), np.zeros(2, np.float32),
+                           np.zeros(2, np.float32), np.array([100000, 1000], np.float32),
+                           np.array([10, 1000], np.float32), np.zeros(2, np.float32),
+                           np.zeros(2, np.float32))
+    r = oracle.assign([[0.5]], [[1.0]], [50000], inst, (0, 1, 0))
+    assert r["assign"].tolist() == [0]
+    r = oracle.assign([[0.5]], [[500.0]], [10], inst, (0, 1, 0))
+    assert r["assign"].tolist() == [1]
+    # queued work counts: the same request avoids an instance with a long queue
+    inst2 = inst.copy()
+    inst2.prefill_rate[:] = 1000
+    inst2.decode_rate[:] = 1000
+    inst2.prefill_q[:] = [5000, 0]
+    r = oracle.assign([[0.5]], [[10.0]], [10], inst2, (0, 1, 0))
+    assert r["assign"].tolist() == [1]
+    inst2.prefill_q[:] = [0, 0]
+    inst2.decode_q[:] = [0, 5000]
+    r = oracle.assign([[0.5]], [[10.0]], [10], inst2, (0, 1, 0))
+    assert r["assign"].tolist() == [0]
+
+
+def _random_case(seed, B=24, M=3, I=11):
+    rng = np.random.default_rng(seed)
+    cfg = synth.tiny_config(B=B, M=M, inst_per_model=tuple([I // M + (1 if m < I % M else 0)
+                                                            for m in range(M)]), seed=seed)
+    inst = synth.make_instances(cfg)
+    qh = rng.uniform(0, 1, (B, M))
+    lh = rng.uniform(1, 800, (B, M))
+    pl = rng.integers(1, 3000, B).astype(np.int32)
+    return qh, lh, pl, inst
+
+
+@pytest.mark.parametrize("seed", range(5))
+def test_simplex_corners(seed):
+    qh, lh, pl, inst = _random_case(seed)
+    B, I = qh.shape[0], inst.I
+    # (1,0,0): highest predicted quality of the instance's model, lowest index on ties
+    r = oracle.assign(qh, lh, pl, inst, (1, 0, 0))
+    for b in range(B):
+        vals = qh[b][inst.model]
+        assert r["assign"][b] == int(np.flatnonzero(vals == vals.max())[0])
+    # (0,0,1): cheapest; (0,1,0): fastest at the state seen by that step
+    for w, key in (((0, 0, 1), 2), ((0, 1, 0), 1)):
+        r = oracle.assign(qh, lh, pl, inst, w, trace=True)
+        for b in range(B):
+            S, T, C = oracle.score_row(qh[b], lh[b], pl[b], inst, r["trace_p"][b], r["trace_a"][b],
+                                       w)
+            v = C if key == 2 else T
+            assert r["assign"][b] == int(np.flatnonzero(v == v.min())[0])
+
+
+@pytest.mark.parametrize("seed", range(5))
+def test_score_range_and_scale_invariance(seed):
+    qh, lh, pl, inst = _random_case(seed)
+    w = (0.2, 0.5, 0.3)
+    S0 = oracle.score(qh, lh, pl, inst, w)
+    assert np.all(S0 >= -1e-12) and np.all(S0 <= 1 + 1e-12)
+    scaled = inst.copy()
+    scaled.price_in = (inst.price_in.astype(np.float64) * 3.0)
+    scaled.price_out = (inst.price_out.astype(np.float64) * 3.0)
+    np.testing.assert_allclose(oracle.score(qh, lh, pl, scaled, w), S0, rtol=1e-12, atol=1e-14)
+    scaled = inst.copy()
+    scaled.prefill_rate = inst.prefill_rate.astype(np.float64) * 0.25
+    scaled.decode_rate = inst.decode_rate.astype(np.float64) * 0.25
+    np.testing.assert_allclose(oracle.score(qh, lh, pl, scaled, w), S0, rtol=1e-12, atol=1e-14)
+
+
+@pytest.mark.parametrize("seed", range(5))
+def test_greedy_invariants(seed):
+    qh, lh, pl, inst = _random_case(seed)
+    B, I = qh.shape[0], inst.I
+    w = (0.3, 0.4, 0.3)
+    r = oracle.assign(qh, lh, pl, inst, w, trace=True)
+    tp, ta = r["trace_p"], r["trace_a"]
+    # conservation, step by step: only the chosen instance grows, by the prompt
+    # and by the predicted output on its model
+    for b in range(B):
+        i = r["assign"][b]
+        dp = tp[b + 1] - tp[b]
+        da = ta[b + 1] - ta[b]
+        expect_p = np.zeros(I)
+        expect_p[i] = pl[b]
+        expect_a = np.zeros(I)
+        expect_a[i] = lh[b][inst.model[i]]
+        np.testing.assert_allclose(dp, expect_p, rtol=0, atol=1e-9)
+        np.testing.assert_allclose(da, expect_a, rtol=0, atol=1e-9)
+        S, _, _ = oracle.score_row(qh[b], lh[b], pl[b], inst, tp[b], ta[b], w)
+        assert i == int(np.argmax(S)) and r["chosen"][b] == S[i]
+    np.testing.assert_array_equal(tp[B], r["p"])
+    # with w_lat = 0 the state never matters: greedy == row-wise argmax of S0
+    w0 = (0.6, 0.0, 0.4)
+    r0 = oracle.assign(qh, lh, pl, inst, w0)
+    S0 = oracle.score(qh, lh, pl, inst, w0)
+    assert r0["assign"].tolist() == np.argmax(S0, axis=1).tolist()
+    # B = 1 is the argmax of S0's first row
+    r1 = oracle.assign(qh[:1], lh[:1], pl[:1], inst, w)
+    S1 = oracle.score(qh[:1], lh[:1], pl[:1], inst, w)
+    assert r1["assign"][0] == int(np.argmax(S1[0]))
+
+
+def test_zero_cost_maximum():
+    # all prices zero: the cost term contributes w_cost to every instance
+    qh, lh, pl, inst = _random_case(11, B=3)
+    inst.price_in[:] = 0
+    inst.price_out[:] = 0
+    w = (0.0, 0.0, 1.0)
+    S0 = oracle.score(qh, lh, pl, inst, w)
+    assert np.all(S0 == 1.0)
+    r = oracle.assign(qh, lh, pl, inst, w)
+    assert r["assign"].tolist() == [0, 0, 0]
+
+
+# ----------------------------------------------------------------------------- carry
+
+
+def test_advance_closed_form():
+    p = np.array([100.0, 0.0, 5000.0])
+    a = np.array([1000.0, 10.0, 0.0])
+    P = np.array([1000.0, 500.0, 2000.0])
+    D = np.array([50.0, 100.0, 10.0])
+    p1, a1 = oracle.advance(p, a, P, D, 0.0)
+    assert np.array_equal(p1, p) and np.array_equal(a1, a)
+    p1, a1 = oracle.advance(p, a, P, D, 0.5)
+    # 100 - 500 clamps to 0; 5000 - 1000 = 4000; 1000 - 25 = 975; 10 - 50 clamps; 0 stays
+    assert p1.tolist() == [0.0, 0.0, 4000.0]
+    assert a1.tolist() == [975.0, 0.0, 0.0]
+    with pytest.raises(ValueError):
+        oracle.advance(p, a, P, D, -1.0)
