@@ -1,0 +1,217 @@
+"""Benchmark of the batched routing path on one MI355X.
+
+A step is one pass of the whole hot path over one batch: exact k-NN of the
+batch's request embeddings against the reference bank, the KNN-averaged
+quality and length predictions, the greedy assignment with dead-reckoned
+instance state (one fused rb_route_batch call), then the carry of the state to
+the next batch (rb_advance_state, 1/30 s per request). Inputs are synthetic and
+already resident in HBM when the timed region starts.
+
+Default workload: the high-load batch, B=256 requests, N=1,000,000 bank rows,
+d=768 bf16 (1.5 GB), M=4 models, I=13 instances, k=10, weights (1/3,1/3,1/3),
+100 consecutive batches. ``--workload`` selects another of the synthetic
+workloads (tiny, online, highload, largebatch, wide).
+
+Prints one JSON line with decisions/s (value), the bank-scan bandwidth, the
+roofline of the bank-scan kernel (timed with HIP events on its own stream) and
+the CPU oracle's rate on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0      # dense bf16 MFMA
+FP32_PEAK_TFLOPS = 157.3
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="highload")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample", type=int, default=0,
+                    help="requests in the CPU oracle sample (0: 8 per host thread)")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a plain device copy of 1 GiB (counter calibration)")
+    return ap.parse_args()
+
+
+def calibrate_copy():
+    import torch
+    n = 1 << 30
+    a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    b = torch.empty(n, dtype=torch.uint8, device="cuda")
+    a.fill_(1)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibrate_copy_bytes": n, "launches": 3}), flush=True)
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the bank-sharded multi-GPU design is described in DESIGN.md).", file=sys.stderr)
+        sys.exit(2)
+    if args.calibrate_copy:
+        calibrate_copy()
+        return
+
+    import numpy as np
+    import torch
+
+    import paper_2606_17949_amd as rb
+    import synth
+
+    cfg = synth.CONFIGS[args.workload]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    K, W = args.steps, args.warmup
+    nb = K + W
+    log(f"workload {cfg.name}: B={cfg.B} N={cfg.N} d={cfg.d} {cfg.dtype} M={cfg.M} I={cfg.I} "
+        f"k={cfg.k}, {W} warm-up + {K} timed batches")
+
+    t0 = time.time()
+    centres = synth.make_centres(cfg, dev)
+    bank = synth.make_bank(cfg, dev, centres)
+    queries = [synth.make_queries(cfg, t, dev, centres) for t in range(nb)]
+    qual, length = synth.make_labels(cfg)
+    plens = [torch.from_numpy(synth.make_prompt_lens(cfg, t)).to(dev) for t in range(nb)]
+    inst_h = synth.make_instances(cfg)
+    g_qual = torch.from_numpy(qual).to(dev)
+    g_len = torch.from_numpy(length).to(dev)
+    inst = rb.DeviceInstances.from_host(inst_h, dev)
+    norms = rb.rb_bank_norms(bank)
+    dt_code = rb.RB_BF16 if cfg.dtype == "bf16" else rb.RB_F32
+    ws = rb.workspace(cfg.B, cfg.N, cfg.d, dt_code, cfg.k, cfg.M, dev)
+    assign = torch.empty(nb, cfg.B, dtype=torch.int32, device=dev)
+    carry_dt = cfg.B / 30.0
+    torch.cuda.synchronize()
+    log(f"inputs resident in HBM ({time.time() - t0:.1f}s); bank {cfg.bank_bytes() / 1e9:.3f} GB")
+
+    stream = torch.cuda.current_stream()
+    ev_b = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+    ev_e = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+    for ev in ev_b + ev_e:      # torch creates the HIP event on first record
+        ev.record(stream)
+
+    def step(t):
+        rb.rb_route_batch(queries[t], bank, norms, cfg.k, g_qual, g_len, plens[t], inst,
+                          cfg.weights, ws=ws, assign=assign[t], stream=stream)
+        rb.rb_advance_state(inst, carry_dt, stream=stream)
+
+    for t in range(W):
+        step(t)
+    torch.cuda.synchronize()
+    log("warm-up done")
+
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    w0 = time.perf_counter()
+    for j in range(K):
+        rb.rb_profile_scan_events(ev_b[j], ev_e[j])
+        step(W + j)
+    rb.rb_profile_scan_events(None, None)
+    end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    total_ms = start.elapsed_time(end)
+    scan_ms = [ev_b[j].elapsed_time(ev_e[j]) for j in range(K)]
+    scan_avg = float(np.mean(scan_ms))
+    log(f"timed {K} batches: {total_ms:.3f} ms (events), {wall * 1e3:.3f} ms (host wall); "
+        f"scan kernel avg {scan_avg * 1e3:.1f} us")
+
+    ms_per_step = total_ms / K
+    decisions = cfg.B * K / (total_ms / 1e3)
+    bank_bytes = cfg.bank_bytes()
+    scan_gbs = bank_bytes / (scan_avg / 1e3) / 1e9
+    flops = 2.0 * cfg.B * cfg.N * cfg.d
+    ai = flops / bank_bytes
+    peak_tf = BF16_PEAK_TFLOPS if cfg.dtype == "bf16" else FP32_PEAK_TFLOPS
+    ridge = peak_tf * 1e12 / (HBM_PEAK_GBS * 1e9)
+    if ai < ridge:
+        roof = {"bound": "hbm", "achieved": round(scan_gbs, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(scan_gbs / HBM_PEAK_GBS, 4), "traffic": None}
+    else:
+        tf = flops / (scan_avg / 1e3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(tf, 1), "peak": peak_tf, "unit": "TFLOP/s",
+                "frac": round(tf / peak_tf, 4), "traffic": None}
+    roof["kernel"] = "scan_kernel (bank distance contraction + fused per-chunk top-k)"
+    roof["per_launch"] = {"bytes": bank_bytes, "flops": flops, "avg_us": round(scan_avg * 1e3, 2),
+                          "p10_us": round(float(np.percentile(scan_ms, 10)) * 1e3, 2),
+                          "p90_us": round(float(np.percentile(scan_ms, 90)) * 1e3, 2)}
+    roof["mfma_tflops"] = round(flops / (scan_avg / 1e3) / 1e12, 1)
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(cfg, bank, queries[W], qual, length, plens[W].cpu().numpy(), inst_h,
+                           args.cpu_sample)
+
+    out = {
+        "metric": "routing decisions/sec + bank-scan HBM GB/s (B=256, N=1M, d=768)",
+        "value": round(decisions, 1),
+        "unit": "decisions/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic (seeded Gaussian-mixture embeddings, Beta/LogNormal labels)",
+        "config": {"workload": f"{cfg.name}: B={cfg.B} N={cfg.N} d={cfg.d} {cfg.dtype} bank, "
+                               f"M={cfg.M} I={cfg.I} k={cfg.k}, {K} carried batches",
+                   "B": cfg.B, "N": cfg.N, "d": cfg.d, "k": cfg.k, "M": cfg.M, "I": cfg.I,
+                   "weights": [round(w, 6) for w in cfg.weights], "carry_dt_s": round(carry_dt, 6),
+                   "parallelism": "single GPU"},
+        "bank_scan_gbps": round(scan_gbs, 1),
+        "arith_intensity_flop_per_byte": round(ai, 1),
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(cfg, bank, queries, qual, length, plen, inst_h, sample):
+    """The oracle as it stands on a bounded sample: the first S requests of the
+    first timed batch, full k-NN over the whole bank, predictions and the greedy
+    assignment, on all host threads available to this process."""
+    import numpy as np
+
+    import oracle
+    threads = len(os.sched_getaffinity(0))
+    S = sample if sample > 0 else min(cfg.B, 8 * threads)
+    log(f"cpu baseline: oracle on {S} requests, {threads} threads ...")
+    bank_h = bank.cpu()
+    q_h = queries[:S].cpu()
+    t0 = time.perf_counter()
+    idx, _ = oracle.knn(q_h, bank_h, cfg.k, nthreads=threads)
+    qh, lh = oracle.predict(idx, qual, length)
+    oracle.assign(qh, lh, plen[:S], inst_h, cfg.weights)
+    dt = time.perf_counter() - t0
+    log(f"cpu baseline: {dt:.1f}s")
+    return {"value": round(S / dt, 3), "unit": "decisions/s", "cores": threads, "kind": "oracle",
+            "sample": f"first {S} requests of one {cfg.B}-request batch: exact fp64 k-NN over "
+                      f"all {cfg.N} bank rows, predictions, greedy assignment ({dt:.1f} s)"}
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,211 @@
+/*
+ * routebalance.h -- C ABI of the MI355X (gfx950) batched request-to-instance
+ * scoring path of RouteBalance (arXiv 2606.17949).
+ *
+ * For a batch of requests the library
+ *   1. finds the k nearest reference prompts of each request embedding in a
+ *      labelled bank (Sec. 4.2, the KNN lookup of Alg. 1),
+ *   2. averages the neighbours' per-model quality and output-length labels into
+ *      predictions Q[r][m], L[r][m] (Sec. 4.2),
+ *   3. scores every request-instance pair with Eq. 1, using the cost of Eq. 2
+ *      and a latency dead-reckoned from instance state (Sec. 4.2), and
+ *   4. assigns each request to one instance greedily, updating the chosen
+ *      instance's state before the next request is scored (Alg. 1, Sec. 4.1).
+ *
+ * Conventions shared by every entry point
+ *   - Every pointer argument is a DEVICE pointer unless stated otherwise; the
+ *     struct arguments themselves (rb_instances, rb_weights) live on the host.
+ *   - The caller owns and allocates every buffer, including the workspace. The
+ *     library never allocates, frees, copies to the host or synchronises; it
+ *     keeps no state between calls beyond a per-device cache of the compute
+ *     unit count. Work is enqueued on `stream` (a hipStream_t; NULL = the null
+ *     stream) and runs asynchronously.
+ *   - Arrays are row-major; "[X][Y]" means Y is contiguous.
+ *   - All arguments are validated on the host before anything is enqueued. On
+ *     any error nothing is enqueued and no output is touched.
+ *   - Faults inside kernels surface at the caller's next synchronisation.
+ *   - Values that live in device memory are not checked (documented
+ *     preconditions): rates > 0, prices >= 0, prompt lengths >= 1, model ids in
+ *     [0, M), embeddings, norms and labels finite. Violating them is undefined.
+ *   - Results are deterministic: the same inputs give bit-identical outputs on
+ *     every call.
+ */
+#ifndef ROUTEBALANCE_H
+#define ROUTEBALANCE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    RB_OK = 0,
+    RB_ERR_NULL = -1,        /* a required pointer is NULL */
+    RB_ERR_DIMS = -2,        /* a size is out of range (see each call) */
+    RB_ERR_DTYPE = -3,       /* dtype is not RB_F32 or RB_BF16 */
+    RB_ERR_WEIGHTS = -4,     /* weights not finite, negative, or |sum - 1| > 1e-5 */
+    RB_ERR_WORKSPACE = -5,   /* workspace NULL or smaller than rb_workspace_size */
+    RB_ERR_UNSUPPORTED = -6, /* an option this version does not implement */
+    RB_ERR_HIP = -7,         /* a HIP runtime call or kernel launch failed */
+    RB_ERR_ALIGN = -8        /* a pointer is not aligned as required */
+} rb_status;
+
+typedef enum { RB_F32 = 0, RB_BF16 = 1 } rb_dtype;
+
+/* Neighbour-averaging rule for rb_predict. Sec. 4.2 calls the paper's KNN
+ * "distance-weighted" without giving the weights; this version implements the
+ * uniform mean only and returns RB_ERR_UNSUPPORTED for anything else. */
+typedef enum { RB_KNN_UNIFORM = 0 } rb_knn_weighting;
+
+#define RB_MAX_K 64      /* largest neighbour count k */
+#define RB_MAX_D 2048    /* largest embedding dimension d */
+#define RB_MAX_I 1024    /* largest instance count I */
+#define RB_MAX_M 1024    /* largest model count M */
+
+/* Scheduling weights on the 3-simplex, in the order of Alg. 1:
+ * (w_qual, w_lat, w_cost), each >= 0, summing to 1 within 1e-5. */
+typedef struct {
+    float w_qual, w_lat, w_cost;
+} rb_weights;
+
+/* Instance table (Tab. notation: instances I, model m(i)), a host struct of
+ * device pointers, each array of length I:
+ *   model        int32, m(i) in [0, M)
+ *   prefill_q    fp32, queued prefill tokens p_i          (IN/OUT, dead reckoning)
+ *   decode_q     fp32, active decode tokens a_i           (IN/OUT, dead reckoning)
+ *   prefill_rate fp32, prefill tokens/s P_i > 0
+ *   decode_rate  fp32, decode tokens/s D_i > 0
+ *   price_in     fp32, price per input token  (c_in of Eq. 2)  >= 0
+ *   price_out    fp32, price per output token (c_out of Eq. 2) >= 0
+ * Latency of request r on instance i (the state-and-rate form of the estimate
+ * in Sec. 4.2): T = (p_i + l_r)/P_i + (a_i + L[r][m(i)])/D_i.
+ * Cost (Eq. 2): C = l_r*price_in[i] + L[r][m(i)]*price_out[i]. */
+typedef struct {
+    const int32_t *model;
+    float *prefill_q;
+    float *decode_q;
+    const float *prefill_rate;
+    const float *decode_rate;
+    const float *price_in;
+    const float *price_out;
+} rb_instances;
+
+/* Human-readable name of a status code (static storage, never NULL). */
+const char *rb_status_string(rb_status s);
+
+/* Bytes of device workspace that rb_knn_topk and rb_route_batch need for these
+ * sizes on the current device, written to *bytes (a host pointer). The value
+ * depends on the device's compute-unit count; query it on the device that will
+ * run the call. Errors: RB_ERR_NULL (bytes), RB_ERR_DIMS / RB_ERR_DTYPE as for
+ * rb_knn_topk, RB_ERR_HIP if the device cannot be queried. */
+rb_status rb_workspace_size(int B, int N, int d, rb_dtype dtype, int k, int M, size_t *bytes);
+
+/* Squared L2 norms of the bank rows, norms[n] = sum_t bank[n][t]^2 in fp32
+ * (a fixed summation order, so the result is reproducible).
+ * The reference bank is static, so this is computed once when the bank is
+ * loaded and passed to every rb_knn_topk / rb_route_batch call.
+ *   bank  [N][d] of dtype (16-byte aligned); norms [N] fp32 (output).
+ * Errors: RB_ERR_NULL, RB_ERR_DTYPE, RB_ERR_DIMS (N < 1, d < 1, d > RB_MAX_D,
+ * d % 8 for bf16 or d % 4 for fp32 not 0), RB_ERR_ALIGN, RB_ERR_HIP. */
+rb_status rb_bank_norms(const void *bank, rb_dtype dtype, int N, int d, float *norms,
+                        void *stream);
+
+/* Exact k-nearest-neighbour search (Sec. 4.2: each request embedding is looked
+ * up against the labelled reference bank with k = 10 in the paper).
+ * Distance: squared Euclidean, computed as |q|^2 + |x|^2 - 2<q, x> with fp32
+ * products and accumulation (bf16 x bf16 products are exact in fp32). Order:
+ * distance ascending, equal distances by the lower bank index.
+ *   queries    [B][d] of dtype. For a bf16 bank the caller rounds the queries
+ *              to bf16 (round to nearest even) before the call.
+ *   bank       [N][d] of dtype; bank_norms [N] fp32 from rb_bank_norms.
+ *   nbr_idx    [B][k] int32 (output): bank row indices, nearest first.
+ *   nbr_dist   [B][k] fp32  (output): their squared distances; may be NULL.
+ *   ws         device workspace of ws_bytes >= rb_workspace_size(...), 256-byte
+ *              aligned; its contents on entry do not matter.
+ * B = 0 enqueues nothing and returns RB_OK.
+ * Errors: RB_ERR_NULL; RB_ERR_DTYPE; RB_ERR_DIMS (B < 0, N < 1, k < 1,
+ * k > min(N, RB_MAX_K), d < 1, d > RB_MAX_D, d % 8 for bf16 or d % 4 for fp32
+ * not 0); RB_ERR_ALIGN (queries, bank not 16-byte aligned, ws not 256-byte
+ * aligned); RB_ERR_WORKSPACE; RB_ERR_HIP. */
+rb_status rb_knn_topk(const void *queries, const void *bank, const float *bank_norms,
+                      rb_dtype dtype, int B, int N, int d, int k, int32_t *nbr_idx,
+                      float *nbr_dist, void *ws, size_t ws_bytes, void *stream);
+
+/* KNN-averaged predictions (Sec. 4.2: each neighbour stores a quality label and
+ * an output length for every model, so one lookup predicts both for every
+ * candidate model). With RB_KNN_UNIFORM:
+ *   q_hat[b][m] = (1/k) * sum_j bank_qual[nbr_idx[b][j]][m]
+ *   l_hat[b][m] = (1/k) * sum_j bank_len [nbr_idx[b][j]][m]
+ * summed in fp32 in neighbour order j = 0..k-1.
+ *   nbr_idx [B][k] int32 in [0, N); nbr_dist [B][k] fp32, unused by the uniform
+ *   rule and may be NULL; bank_qual, bank_len [N][M] fp32;
+ *   q_hat, l_hat [B][M] fp32 (outputs).
+ * Errors: RB_ERR_NULL, RB_ERR_DIMS (B < 0, k < 1, k > RB_MAX_K, N < 1, M < 1,
+ * M > RB_MAX_M), RB_ERR_UNSUPPORTED (weighting), RB_ERR_HIP. */
+rb_status rb_predict(const int32_t *nbr_idx, const float *nbr_dist, int B, int k,
+                     rb_knn_weighting weighting, const float *bank_qual, const float *bank_len,
+                     int N, int M, float *q_hat, float *l_hat, void *stream);
+
+/* Dense score matrix at the instances' current state (Eq. 1 for every pair):
+ *   S0[r][i] = w_qual*Q[r][m(i)] + w_cost*(1 - C[r][i]/max_j C[r][j])
+ *            + w_lat *(1 - T[r][i]/max_j T[r][j])
+ * with C and T as in rb_instances; a zero maximum makes its ratio 0. The state
+ * is read, not modified. fp32 arithmetic.
+ *   q_hat, l_hat [B][M] fp32; prompt_len [B] int32 (input tokens l_r >= 1);
+ *   inst: host struct of device arrays of length I; score0 [B][I] fp32 (output).
+ * Errors: RB_ERR_NULL, RB_ERR_DIMS (B < 0, M < 1, M > RB_MAX_M, I < 1,
+ * I > RB_MAX_I), RB_ERR_WEIGHTS, RB_ERR_HIP. */
+rb_status rb_score(const float *q_hat, const float *l_hat, const int32_t *prompt_len, int B,
+                   int M, const rb_instances *inst, int I, rb_weights w, float *score0,
+                   void *stream);
+
+/* Greedy online assignment in arrival order (Alg. 1 loop; Sec. 4.1; the
+ * dead-reckoning update of Sec. 4.2). For r = 0..B-1: score request r against
+ * every instance at the CURRENT state (as rb_score does for one row), pick
+ * i* = argmax (the lowest index among exactly equal scores), then
+ *   prefill_q[i*] += l_r;  decode_q[i*] += L[r][m(i*)].
+ * Rates and prices are unchanged. Runs on one wavefront, fp32.
+ *   assign [B] int32 (output); chosen_score [B] fp32 (output, may be NULL);
+ *   inst->prefill_q / decode_q are updated in place.
+ * Errors: as rb_score, plus RB_ERR_NULL for assign. */
+rb_status rb_assign(const float *q_hat, const float *l_hat, const int32_t *prompt_len, int B,
+                    int M, const rb_instances *inst, int I, rb_weights w, int32_t *assign,
+                    float *chosen_score, void *stream);
+
+/* The whole path for one batch: rb_knn_topk, then rb_predict (uniform), then
+ * rb_assign, enqueued back to back on `stream`. The intermediate outputs
+ * nbr_idx [B][k], nbr_dist [B][k], q_hat [B][M], l_hat [B][M] and
+ * chosen_score [B] are written when their pointers are non-NULL and otherwise
+ * kept in the workspace. inst state is updated in place as by rb_assign.
+ * Errors: the union of those of the three calls. */
+rb_status rb_route_batch(const void *queries, const void *bank, const float *bank_norms,
+                         rb_dtype dtype, int B, int N, int d, int k, const float *bank_qual,
+                         const float *bank_len, int M, const int32_t *prompt_len,
+                         const rb_instances *inst, int I, rb_weights w, int32_t *assign,
+                         float *chosen_score, int32_t *nbr_idx, float *nbr_dist, float *q_hat,
+                         float *l_hat, void *ws, size_t ws_bytes, void *stream);
+
+/* Carry the dead-reckoned state across a gap of dt_seconds between batches:
+ *   prefill_q[i] = max(0, prefill_q[i] - prefill_rate[i]*dt)
+ *   decode_q[i]  = max(0, decode_q[i]  - decode_rate[i]*dt)
+ * (a clamped linear drain; the paper re-reads telemetry per batch instead).
+ * Errors: RB_ERR_NULL, RB_ERR_DIMS (I < 1, I > RB_MAX_I, dt not finite or < 0),
+ * RB_ERR_HIP. */
+rb_status rb_advance_state(const rb_instances *inst, int I, float dt_seconds, void *stream);
+
+/* Timing hook for the bank scan, the dominant kernel of rb_knn_topk and
+ * rb_route_batch. While set, every later call of those two entry points made
+ * from the calling host thread records `begin` (a hipEvent_t) on the call's
+ * stream immediately before the bank-scan kernel and `end` immediately after
+ * it, so hipEventElapsedTime(begin, end) is that kernel's duration. Pass NULL,
+ * NULL to stop. The setting is per host thread; the events stay owned by the
+ * caller. Always returns RB_OK. */
+rb_status rb_profile_scan_events(void *begin, void *end);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ROUTEBALANCE_H */

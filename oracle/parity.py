@@ -1,0 +1,142 @@
+"""Acceptance checks: GPU outputs against the CPU oracle.
+
+TEST INFRASTRUCTURE ONLY (tests, smoke check, benchmark baseline). Takes numpy
+arrays; never imports the GPU package.
+
+Tolerances (floating point fixed at 1e-5 relative for decisions and 1e-4 for
+values):
+  rel(a, b) = |a - b| / max(|a|, |b|, f), f = 1 for squared distances of
+  unit-scale embeddings (fp32 cancellation in |q|^2 + |x|^2 - 2<q,x> is
+  absolute, about 1e-6 at d = 768), f = 1e-6 otherwise.
+  * neighbours: an index in one list but not the other must sit within 1e-5 of
+    the oracle's k-th distance (a boundary near-tie); order may differ only
+    among near-equal distances; GPU distances of listed rows within 1e-5.
+  * predictions: teacher-forced, recomputed by the oracle from the GPU's own
+    neighbour list, within 1e-4.
+  * scores: from the GPU's predictions, within 1e-4.
+  * assignment: teacher-forced replay; each GPU pick must be the oracle's pick
+    or score within 1e-5 of the oracle's best (a near tie, counted); the
+    replay continues with the GPU's pick; the state after the batch within
+    1e-4. Free-running (the oracle on its own): bit-identical picks when the
+    replay saw no near tie.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from . import assign as _assign, knn as _knn, predict as _predict, score as _score, \
+    score_row as _score_row
+
+DIST_RTOL = 1e-5
+DIST_FLOOR = 1.0
+VAL_RTOL = 1e-4
+VAL_FLOOR = 1e-6
+PICK_RTOL = 1e-5
+
+
+def rel(a, b, floor):
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    return np.abs(a - b) / np.maximum(np.maximum(np.abs(a), np.abs(b)), floor)
+
+
+def check_neighbours(g_idx, g_dist, o_idx, o_dist, rows=None, label=""):
+    """Compare per-request neighbour lists. ``rows`` maps row i of the oracle
+    arrays to row rows[i] of the GPU arrays (sampled checks). Returns the number
+    of boundary near-tie substitutions."""
+    g_idx = np.asarray(g_idx)
+    g_dist = None if g_dist is None else np.asarray(g_dist, np.float64)
+    o_idx = np.asarray(o_idx)
+    o_dist = np.asarray(o_dist, np.float64)
+    B, k = o_idx.shape
+    rows = np.arange(B) if rows is None else np.asarray(rows)
+    ties = 0
+    for i in range(B):
+        gi = g_idx[rows[i]]
+        oi = o_idx[i]
+        od = dict(zip(oi.tolist(), o_dist[i].tolist()))
+        kth = o_dist[i, -1]
+        assert len(set(gi.tolist())) == k, f"{label} row {rows[i]}: duplicate indices {gi}"
+        only_g = set(gi.tolist()) - set(oi.tolist())
+        only_o = set(oi.tolist()) - set(gi.tolist())
+        for j in only_o:
+            assert rel(od[j], kth, DIST_FLOOR) <= DIST_RTOL, \
+                f"{label} row {rows[i]}: oracle neighbour {j} (d={od[j]}) missing, k-th {kth}"
+        if g_dist is not None:
+            gd = g_dist[rows[i]]
+            for pos, j in enumerate(gi.tolist()):
+                if j in od:
+                    assert rel(gd[pos], od[j], DIST_FLOOR) <= DIST_RTOL, \
+                        f"{label} row {rows[i]}: idx {j} gpu d={gd[pos]} oracle d={od[j]}"
+                else:
+                    # a substituted row: its distance must tie the oracle's k-th
+                    assert rel(gd[pos], kth, DIST_FLOOR) <= DIST_RTOL, \
+                        f"{label} row {rows[i]}: extra idx {j} d={gd[pos]} vs k-th {kth}"
+            assert np.all(np.diff(gd) >= -1e-12), f"{label} row {rows[i]}: not sorted {gd}"
+        # order: the GPU list sorted by oracle distance where known must agree up to near ties
+        for pos, j in enumerate(gi.tolist()):
+            if j in od and oi[pos] != j:
+                assert rel(od[j], o_dist[i, pos], DIST_FLOOR) <= DIST_RTOL, \
+                    f"{label} row {rows[i]} pos {pos}: gpu {j} oracle {oi[pos]}"
+        ties += len(only_g)
+    return ties
+
+
+def check_predictions(g_idx, g_qhat, g_lhat, qual, length, label=""):
+    """Teacher-forced: the oracle averages the GPU's own neighbour lists."""
+    qh, lh = _predict(np.asarray(g_idx), qual, length)
+    eq = rel(g_qhat, qh, VAL_FLOOR)
+    el = rel(g_lhat, lh, VAL_FLOOR)
+    assert eq.max() <= VAL_RTOL, f"{label} q_hat rel err {eq.max()}"
+    assert el.max() <= VAL_RTOL, f"{label} l_hat rel err {el.max()}"
+    return float(max(eq.max(), el.max()))
+
+
+def check_scores(g_S0, g_qhat, g_lhat, plen, inst, weights, label=""):
+    S0 = _score(np.asarray(g_qhat, np.float64), np.asarray(g_lhat, np.float64), plen, inst, weights)
+    e = rel(g_S0, S0, VAL_FLOOR)
+    assert e.max() <= VAL_RTOL, f"{label} S0 rel err {e.max()} at {np.unravel_index(e.argmax(), e.shape)}"
+    return float(e.max())
+
+
+def check_assign(g_assign, g_chosen, g_qhat, g_lhat, plen, inst, weights, g_final_p=None,
+                 g_final_a=None, p0=None, a0=None, label=""):
+    """Teacher-forced replay of the greedy loop. Returns the near-tie count."""
+    qh = np.asarray(g_qhat, np.float64)
+    lh = np.asarray(g_lhat, np.float64)
+    g_assign = np.asarray(g_assign)
+    p = np.asarray(inst.prefill_q if p0 is None else p0, np.float64).copy()
+    a = np.asarray(inst.decode_q if a0 is None else a0, np.float64).copy()
+    model = np.asarray(inst.model)
+    ties = 0
+    for r in range(qh.shape[0]):
+        S, _, _ = _score_row(qh[r], lh[r], plen[r], inst, p, a, weights)
+        io = int(np.argmax(S))
+        ig = int(g_assign[r])
+        assert 0 <= ig < S.shape[0], f"{label} step {r}: pick {ig} out of range"
+        if ig != io:
+            gap = S[io] - S[ig]
+            assert gap <= PICK_RTOL * max(abs(S[io]), 1e-6), \
+                f"{label} step {r}: gpu picked {ig} (S={S[ig]}) oracle {io} (S={S[io]})"
+            ties += 1
+        if g_chosen is not None:
+            assert rel(g_chosen[r], S[ig], VAL_FLOOR) <= VAL_RTOL, \
+                f"{label} step {r}: chosen score {g_chosen[r]} vs {S[ig]}"
+        p[ig] += plen[r]
+        a[ig] += lh[r, model[ig]]
+    if g_final_p is not None:
+        e = rel(g_final_p, p, VAL_FLOOR)
+        assert e.max() <= VAL_RTOL, f"{label} final prefill state rel err {e.max()}"
+    if g_final_a is not None:
+        e = rel(g_final_a, a, VAL_FLOOR)
+        assert e.max() <= VAL_RTOL, f"{label} final decode state rel err {e.max()}"
+    return ties
+
+
+def free_running(queries, bank, k, qual, length, plen, inst, weights, nthreads=1):
+    """The oracle alone: its own KNN, predictions and greedy loop."""
+    idx, dist = _knn(queries, bank, k, nthreads=nthreads)
+    qh, lh = _predict(idx, qual, length)
+    res = _assign(qh, lh, plen, inst, weights)
+    res.update(idx=idx, dist=dist, q_hat=qh, l_hat=lh)
+    return res

@@ -27,3 +27,18 @@ def pytest_collection_modifyitems(config, items):
     for it in items:
         if "gpu" in it.keywords:
             it.add_marker(skip)
+
+
+def _ensure_built():
+    """Build the HIP library and the oracle if nothing is built yet."""
+    lib = os.path.join(ROOT, "paper_2606_17949_amd", "librouteb.so")
+    if not os.path.exists(lib):
+        import importlib.util
+        spec = importlib.util.spec_from_file_location(
+            "_rb_build", os.path.join(ROOT, "paper_2606_17949_amd", "build.py"))
+        mod = importlib.util.module_from_spec(spec)
+        spec.loader.exec_module(mod)
+        mod.build()
+
+
+_ensure_built()
