@@ -7,30 +7,37 @@
 
 namespace rb {
 
-constexpr int SCAN_THREADS = 256;         // 4 waves
+constexpr int SCAN_THREADS = 256;   // 4 waves, one per SIMD
 constexpr int SCAN_WAVES = 4;
-constexpr int SCAN_WR = 32;               // bank rows per wave per iteration (two 16-row MFMA tiles)
-constexpr int SCAN_RT = SCAN_WAVES * SCAN_WR;   // bank rows per workgroup iteration
-constexpr int SCAN_DSTRIDE = SCAN_RT + 4; // padded row stride of the distance tile (words)
+constexpr int SCAN_RT = 4;         // 16-row MFMA tiles per wave per iteration (64 rows)
+constexpr int SCAN_PREFETCH = 3;    // k-steps whose loads are in flight ahead of the MFMAs
+constexpr int SCAN_UNROLL = 4;      // register ring of bank fragments; k-steps are padded to it
+constexpr int STAGE_CAP = 256;      // per-wave staging: one (query group, row tile) of candidates
 constexpr size_t LDS_LIMIT = 160 * 1024;
-constexpr int MERGE_THREADS = 256;
-constexpr int MERGE_MAX_EPT = 32;         // partial entries per merge thread
-constexpr int MERGE_MAX_ENTRIES = MERGE_THREADS * MERGE_MAX_EPT;
-constexpr int RB_MAX_K_DEV = 64;          // largest k (the ABI limit)
+constexpr int MERGE_WAVES = 4;      // one query per wave
+constexpr int MERGE_CAP = 1536;     // candidates per query the merge holds in LDS
+constexpr int RB_MAX_K_DEV = 64;    // largest k (the ABI limit)
+constexpr int SEED_MAX_GROUPS = 2048;
 
-// How one rb_knn_topk call is split: query tiles of qt = 16*ng queries, the
-// bank cut into n_chunks contiguous row ranges, one workgroup per
-// (chunk, query tile).
+// How one rb_knn_topk call is split.
+//  * seed: S bank rows spread evenly over the bank; per query, the k-th
+//    smallest of the S/16 minima over groups of 16 of them bounds the k-th
+//    nearest distance from above (k distinct rows lie at or below it).
+//  * scan: query tiles of 16*ng queries; the bank in n_chunks contiguous row
+//    ranges (multiples of 16 rows); one workgroup per (chunk, tile); each of
+//    its 4 waves owns 16*rt rows per iteration and keeps, per query, a list of
+//    at most k candidates that pass the bound.
+//  * merge: per query, the k smallest of its 4*n_chunks lists.
 struct KnnPlan {
     int dtype;          // 0 fp32, 1 bf16
     int B, N, d, k;
-    int ng;             // query groups of 16 per tile (1, 2 or 4)
-    int n_qt;           // query tiles
-    int nks;            // 64-byte k-steps per row
-    int n_chunks;       // bank chunks
+    int nks, nksp;      // 64-byte k-steps per row, padded to SCAN_UNROLL
+    int ng, rt;         // query groups of 16 per tile, 16-row tiles per wave
+    int n_qt, n_chunks, W;
     long rows_per_chunk;
-    size_t lds_bytes;   // dynamic LDS of the scan kernel
-    size_t off_tau, off_pkey, off_pidx, bytes;   // workspace layout
+    int S, G;           // seed rows and groups (0 = no seed)
+    size_t lds_bytes;
+    size_t off_tau, off_qn, off_gmin, off_ccnt, off_ckey, off_cidx, bytes;
 };
 
 int plan_knn(int B, int N, int d, int dtype, int k, int num_cu, KnnPlan *p);

@@ -1,19 +1,26 @@
 // Exact k-nearest-neighbour search over the labelled reference bank
 // (RouteBalance Sec. 4.2: the KNN lookup of Alg. 1), for gfx950.
 //
-// Data flow of one call:
-//   knn_init_kernel   per query: |q|^2 and the shared distance bound <- +inf
-//   scan_kernel       one workgroup per (bank chunk, query tile): bank rows
-//                     stream from HBM straight into MFMA A operands, the query
-//                     tile sits in LDS as MFMA B fragments; each 128-row
-//                     distance tile is filtered against the per-query bound and
-//                     survivors are merged into a per-query top-k list in LDS;
-//                     the chunk's lists go to the workspace
-//   merge_kernel      per query: the k smallest of all chunk lists, sorted,
-//                     optionally followed by the label gather and average
-//                     (Sec. 4.2: one lookup predicts quality and length for
-//                     every model)
-// Order everywhere: distance ascending, equal distances by the lower bank index.
+// Kernels of one call:
+//   seed_groups_kernel  distances of every query to S bank rows spread evenly
+//                       over the bank; minima over groups of 16 of those rows
+//   seed_bound_kernel   per query: |q|^2, and the k-th smallest group minimum
+//                       as the starting bound of the k-th nearest distance
+//   scan_kernel         the bank once through MFMA: one workgroup per (bank
+//                       chunk, tile of up to 256 queries); bank rows go from
+//                       HBM straight into MFMA operand registers, the query
+//                       tile streams through an LDS double buffer along K; a
+//                       register-level test against the per-query bound lets
+//                       only candidates reach the per-wave top-k lists
+//   merge_kernel        per query: the k nearest of all lists, sorted, then
+//                       optionally the label gather and average (Sec. 4.2: one
+//                       lookup predicts quality and length for every model)
+// Order everywhere: distance ascending, equal distances by the lower bank
+// index. Distances are |q|^2 + |x|^2 - 2<q,x> with fp32 products and
+// accumulation; the scan accumulates -|x|^2/2 + <q,x> and reports
+// |q|^2 - 2*acc.
+#include <float.h>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -21,11 +28,11 @@ namespace rb {
 
 namespace {
 
-constexpr int KB = 8;   // k-steps whose bank loads are issued together
-
 template <int DT> struct Elem;
 template <> struct Elem<0> { static constexpr int VEC = 4, ESZ = 4; };   // fp32
 template <> struct Elem<1> { static constexpr int VEC = 8, ESZ = 2; };   // bf16
+
+constexpr int KSTEP_BYTES = 64;   // bytes of one row in one k-step (4 lanes x 16 bytes)
 
 // Sum of squares of the 16-byte group held in v, added to s in element order.
 template <int DT>
@@ -49,24 +56,101 @@ __device__ __forceinline__ float sumsq16(const i32x4 &v, float s)
     return s;
 }
 
-// One 16x16 MFMA tile step over 16 bytes of K per lane:
+// One 16x16 MFMA tile step over 16 bytes of K per lane, D = A*B + C:
 //   bf16: one v_mfma_f32_16x16x32_bf16 (8 elements per lane)
 //   fp32: four v_mfma_f32_16x16x4_f32 (element e of every lane in step e)
 // A and B hold the same K positions in the same lanes, so the dot products
 // come out right whatever order the hardware assigns K within a step.
 template <int DT>
-__device__ __forceinline__ void mfma_step(const i32x4 &a, const i32x4 &b, f32x4 &c)
+__device__ __forceinline__ f32x4 mfma_step(const i32x4 &a, const i32x4 &b, const f32x4 &c)
 {
     if constexpr (DT == 1) {
-        c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
-                                                    __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                       __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
     } else {
+        f32x4 d = c;
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-            c = __builtin_amdgcn_mfma_f32_16x16x4f32(__int_as_float(a[e]), __int_as_float(b[e]), c,
+            d = __builtin_amdgcn_mfma_f32_16x16x4f32(__int_as_float(a[e]), __int_as_float(b[e]), d,
                                                      0, 0, 0);
+        return d;
     }
 }
+
+__device__ __forceinline__ i32x4 load16(const uint8_t *p) { return *(const i32x4 *)p; }
+
+template <int I> struct Int {
+    static constexpr int value = I;
+};
+
+// f(Int<I>) for I = B..E-1, unrolled at compile time.
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F &&f)
+{
+    if constexpr (B < E) {
+        f(Int<B>{});
+        static_for<B + 1, E>(f);
+    }
+}
+
+// Workgroup barrier that orders LDS only (waits for this wave's LDS traffic),
+// leaving global loads in flight across it.
+__device__ __forceinline__ void lds_barrier()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+__device__ __forceinline__ uint32_t lds_load_relaxed(const uint32_t *p)
+{
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+__device__ __forceinline__ void lds_store_relaxed(uint32_t *p, uint32_t v)
+{
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+__device__ __forceinline__ uint64_t pack(uint32_t key, int32_t idx)
+{
+    return ((uint64_t)key << 32) | (uint32_t)idx;
+}
+
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v)
+{
+#pragma unroll
+    for (int m = 1; m < WAVE; m <<= 1) {
+        const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, m);
+        const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), m);
+        const uint64_t o = ((uint64_t)hi << 32) | lo;
+        v = o > v ? o : v;
+    }
+    return v;
+}
+
+// Inclusive prefix sum over the wave.
+__device__ __forceinline__ int wave_incl_scan(int v)
+{
+    const int lane = lane_id();
+#pragma unroll
+    for (int m = 1; m < WAVE; m <<= 1) {
+        const int o = __shfl_up(v, m);
+        if (lane >= m)
+            v += o;
+    }
+    return v;
+}
+
+__device__ __forceinline__ int wave_sum_int(int v)
+{
+#pragma unroll
+    for (int m = 1; m < WAVE; m <<= 1)
+        v += __shfl_xor(v, m);
+    return v;
+}
+
+// ------------------------------------------------------------------ norms
 
 // Squared norms of rows, one wave per row, 16-byte lanes, fixed reduction tree.
 template <int DT>
@@ -81,98 +165,161 @@ __global__ __launch_bounds__(256) void bank_norms_kernel(const uint8_t *__restri
         const uint8_t *row = bank + n * row_bytes;
         float s = 0.f;
         for (int off = lane * 16; off < row_bytes; off += WAVE * 16)
-            s = sumsq16<DT>(*(const i32x4 *)(row + off), s);
+            s = sumsq16<DT>(load16(row + off), s);
         s = wave_sum(s);
         if (lane == 0)
             norms[n] = s;
     }
 }
 
-// Per query: |q|^2 (same arithmetic as the bank norms) and the shared bound.
+// ------------------------------------------------------------------ seed
+
+struct SeedArgs {
+    const uint8_t *queries, *bank;
+    const float *bank_norms;
+    int B, N, d, nks, S, G, n_qg;
+    float *gmin;   // [B][G]
+};
+
+// Bank row of seed sample j: S rows spread evenly over [0, N).
+__device__ __forceinline__ long seed_row(int j, int N, int S)
+{
+    return (long)j * N / S;
+}
+
+// One wave per (query group of 16, block of 64 sample rows): partial distances
+// p = |x|^2 - 2<q,x> by MFMA, then each lane's minimum over its 16 rows.
 template <int DT>
-__global__ __launch_bounds__(256) void knn_init_kernel(const uint8_t *__restrict__ queries, int B,
-                                                       int d, float *__restrict__ qn,
-                                                       uint32_t *__restrict__ tau)
+__global__ __launch_bounds__(256) void seed_groups_kernel(const SeedArgs A)
+{
+    constexpr int VEC = Elem<DT>::VEC, ESZ = Elem<DT>::ESZ;
+    const int lane = lane_id(), col = lane & 15, jg = lane >> 4;
+    const int wid = (int)(((long)blockIdx.x * blockDim.x + threadIdx.x) >> 6);
+    const int qg = wid % A.n_qg, sb = wid / A.n_qg;
+    if (sb >= A.S / 64)
+        return;
+    const size_t rowb = (size_t)A.d * ESZ;
+    const int q = qg * 16 + col;
+    const bool qv = q < A.B;
+    const uint8_t *qp = A.queries + (qv ? (size_t)q * rowb : 0) + jg * 16;
+    const uint8_t *ap[4];
+    f32x4 acc[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        ap[t] = A.bank + (size_t)seed_row(sb * 64 + t * 16 + col, A.N, A.S) * rowb + jg * 16;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            acc[t][e] = -0.5f * A.bank_norms[seed_row(sb * 64 + t * 16 + jg * 4 + e, A.N, A.S)];
+    }
+    for (int s = 0; s < A.nks; ++s) {
+        const bool kv = s * 4 * VEC + jg * VEC < A.d;
+        const i32x4 z = {0, 0, 0, 0};
+        const i32x4 b = kv && qv ? load16(qp + (size_t)s * KSTEP_BYTES) : z;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const i32x4 a = kv ? load16(ap[t] + (size_t)s * KSTEP_BYTES) : z;
+            acc[t] = mfma_step<DT>(a, b, acc[t]);
+        }
+    }
+    float m = INFINITY;
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            m = fminf(m, -2.f * acc[t][e]);
+    if (qv)
+        A.gmin[(size_t)q * A.G + sb * 4 + jg] = m;
+}
+
+// One wave per query: |q|^2, and the starting bound = |q|^2 + the k-th smallest
+// group minimum, widened by a margin far above any fp32 rounding difference
+// between this pass and the scan. Without a seed (G < k) the bound is +inf.
+template <int DT, int GPL>
+__global__ __launch_bounds__(256) void seed_bound_kernel(const uint8_t *__restrict__ queries, int B,
+                                                         int d, int k, const float *__restrict__ gmin,
+                                                         int G, float *__restrict__ qn,
+                                                         uint32_t *__restrict__ tau)
 {
     const int lane = lane_id();
-    const int b = (blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+    const int b = (int)(((long)blockIdx.x * blockDim.x + threadIdx.x) >> 6);
     if (b >= B)
         return;
     const int row_bytes = d * Elem<DT>::ESZ;
     const uint8_t *row = queries + (size_t)b * row_bytes;
     float s = 0.f;
     for (int off = lane * 16; off < row_bytes; off += WAVE * 16)
-        s = sumsq16<DT>(*(const i32x4 *)(row + off), s);
+        s = sumsq16<DT>(load16(row + off), s);
     s = wave_sum(s);
+    uint32_t T = KEY_NONE;
+    if (G >= k) {
+        uint32_t key[GPL];
+#pragma unroll
+        for (int u = 0; u < GPL; ++u) {
+            const int i = lane + WAVE * u;
+            key[u] = i < G ? f2key(gmin[(size_t)b * G + i]) : KEY_NONE;
+        }
+        uint32_t prefix = 0;
+        for (int bit = 31; bit >= 0; --bit) {
+            const uint32_t trial = prefix | (1u << bit);
+            int c = 0;
+#pragma unroll
+            for (int u = 0; u < GPL; ++u)
+                c += key[u] < trial;
+            if (wave_sum_int(c) < k)
+                prefix = trial;
+        }
+        const float pk = key2f(prefix);
+        const float t = s + pk;
+        const float margin = ldexpf(s + fabsf(pk) + 1.f, -14);
+        T = f2key(t + margin);
+    }
     if (lane == 0) {
         qn[b] = s;
-        tau[b] = KEY_NONE;
+        tau[b] = T;
     }
 }
+
+// ------------------------------------------------------------------ scan
 
 struct ScanArgs {
     const uint8_t *queries, *bank;
     const float *bank_norms, *qn;
-    int B, N, d, k, nks, n_chunks, n_qt;
+    int B, N, d, k, nks, nksp, n_chunks, n_qt, W;
     long rows_per_chunk;
-    uint32_t *tau;
-    uint32_t *pkey;
-    int32_t *pidx;
+    uint32_t *tau;    // [B] shared bound (distance keys), lowered with atomicMin
+    int32_t *ccnt;    // [B][W] list lengths
+    uint32_t *ckey;   // [B][W][k]
+    int32_t *cidx;    // [B][W][k]
 };
 
-// Keys of the k smallest entries of the union of three per-lane slots, under
-// (key, index). Returns T, the k-th smallest key, and U: entries with key == T
-// are kept iff their index <= U. Needs at least k valid entries. Bitwise
-// selection from the most significant bit, counting with ballots; the loop
-// bounds and every branch are wave-uniform.
-__device__ __forceinline__ void select_k(uint32_t ka, int32_t ia, bool va, uint32_t kb, int32_t ib,
-                                         bool vb, uint32_t kc, int32_t ic, bool vc, int k,
-                                         uint32_t &T, int32_t &U)
-{
-    uint32_t prefix = 0;
-    for (int bit = 31; bit >= 0; --bit) {
-        const uint32_t trial = prefix | (1u << bit);
-        const int c = popc(ballot(va && ka < trial)) + popc(ballot(vb && kb < trial)) +
-                      popc(ballot(vc && kc < trial));
-        if (c < k)
-            prefix = trial;
-    }
-    T = prefix;
-    const int c_lt = popc(ballot(va && ka < T)) + popc(ballot(vb && kb < T)) +
-                     popc(ballot(vc && kc < T));
-    const int c_eq = popc(ballot(va && ka == T)) + popc(ballot(vb && kb == T)) +
-                     popc(ballot(vc && kc == T));
-    const int r = k - c_lt;
-    U = IDX_NONE;
-    if (c_eq > r) {
-        uint32_t up = 0;
-        for (int bit = 30; bit >= 0; --bit) {
-            const uint32_t trial = up | (1u << bit);
-            const int c = popc(ballot(va && ka == T && (uint32_t)ia < trial)) +
-                          popc(ballot(vb && kb == T && (uint32_t)ib < trial)) +
-                          popc(ballot(vc && kc == T && (uint32_t)ic < trial));
-            if (c < r)
-                up = trial;
-        }
-        U = (int32_t)up;
-    }
-}
-
-template <int DT, int NG>
+template <int DT, int NG, int RT>
 __global__ __launch_bounds__(SCAN_THREADS, 1) void scan_kernel(const ScanArgs A)
 {
-    constexpr int QT = NG * 16;
-    constexpr int VEC = Elem<DT>::VEC;
-    constexpr int ESZ = Elem<DT>::ESZ;
+    constexpr int BM = NG * 16;
+    constexpr int VEC = Elem<DT>::VEC, ESZ = Elem<DT>::ESZ;
+    constexpr int KS = 4 * VEC;                    // elements of one k-step
+    constexpr int RW = RT * 16;                    // rows per wave per iteration
+    constexpr int RWG = SCAN_WAVES * RW;           // rows per workgroup iteration
+    constexpr int QITEMS = NG * WAVE;              // 16-byte query items of one k-step
+    constexpr int QPT = (QITEMS + SCAN_THREADS - 1) / SCAN_THREADS;
+    constexpr int R = SCAN_UNROLL, P = SCAN_PREFETCH;
+    static_assert(P < R, "prefetch distance must leave a free ring slot");
+    static_assert(RW == WAVE, "one bank-norm load per lane per iteration");
+
     extern __shared__ __align__(16) uint8_t smem[];
-    const int k = A.k, nks = A.nks;
-    i32x4 *qfrag = (i32x4 *)smem;                                  // [nks][NG][64]
-    float *qn = (float *)(smem + (size_t)nks * NG * WAVE * 16);    // [QT]
-    uint32_t *dtile = (uint32_t *)(qn + QT);                       // [QT][SCAN_DSTRIDE]
-    uint32_t *lkey = dtile + QT * SCAN_DSTRIDE;                    // [QT][k]
-    int32_t *lidx = (int32_t *)(lkey + QT * k);                    // [QT][k]
-    int *lcnt = (int *)(lidx + QT * k);                            // [QT]
-    uint32_t *ltau = (uint32_t *)(lcnt + QT);                      // [QT]
+    const int k = A.k;
+    i32x4 *qbuf = (i32x4 *)smem;                                    // [2][NG][64]
+    float *qn_s = (float *)(qbuf + 2 * QITEMS);                     // [BM]
+    uint32_t *gb_s = (uint32_t *)(qn_s + BM);                       // [BM] shared-bound snapshot
+    float *nx_all = (float *)(gb_s + BM);                           // [4][2][RW] -|x|^2/2
+    uint32_t *lk_all = (uint32_t *)(nx_all + SCAN_WAVES * 2 * RW);  // [4][BM][k]
+    int32_t *li_all = (int32_t *)(lk_all + SCAN_WAVES * BM * k);    // [4][BM][k]
+    int *lc_all = (int *)(li_all + SCAN_WAVES * BM * k);            // [4][BM]
+    uint32_t *lmk_all = (uint32_t *)(lc_all + SCAN_WAVES * BM);     // [4][BM] max key of a full list
+    int32_t *lmi_all = (int32_t *)(lmk_all + SCAN_WAVES * BM);      // [4][BM] its index
+    int *sq_all = (int *)(lmi_all + SCAN_WAVES * BM);               // [4][STAGE_CAP]
+    uint32_t *sk_all = (uint32_t *)(sq_all + SCAN_WAVES * STAGE_CAP);
+    int32_t *si_all = (int32_t *)(sk_all + SCAN_WAVES * STAGE_CAP);
 
     // Workgroup -> (chunk c, query tile t). Workgroups are dispatched to the
     // eight XCDs round robin, so this map puts every query tile of one chunk
@@ -183,206 +330,305 @@ __global__ __launch_bounds__(SCAN_THREADS, 1) void scan_kernel(const ScanArgs A)
     const int c = (blockIdx.x / per8) * 8 + rem % 8;
     if (c >= A.n_chunks)
         return;
-    const int q0 = t * QT;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int jgrp = lane >> 4, col = lane & 15;
-    const size_t row_bytes = (size_t)A.d * ESZ;
-
-    // Query tile as B fragments: lane l of fragment (s, g) holds query
-    // 16g + l%16, elements [s*4*VEC + (l/16)*VEC, +VEC). Zero past B and d.
-    for (int f = tid; f < nks * NG * WAVE; f += SCAN_THREADS) {
-        const int l = f & 63, g = (f >> 6) % NG, s = f / (NG * WAVE);
-        const int q = q0 + g * 16 + (l & 15);
-        const int kk = s * 4 * VEC + (l >> 4) * VEC;
-        i32x4 v = {0, 0, 0, 0};
-        if (q < A.B && kk < A.d)
-            v = *(const i32x4 *)(A.queries + (size_t)q * row_bytes + (size_t)kk * ESZ);
-        qfrag[f] = v;
-    }
-    for (int q = tid; q < QT; q += SCAN_THREADS) {
-        qn[q] = (q0 + q < A.B) ? A.qn[q0 + q] : 0.f;
-        lcnt[q] = 0;
-        ltau[q] = KEY_NONE;
-    }
-    __syncthreads();
-
+    const int col = lane & 15, jg = lane >> 4;
+    const int q0 = t * BM;
     const long rbeg = (long)c * A.rows_per_chunk;
     const long rend = min((long)A.N, rbeg + A.rows_per_chunk);
-    for (long r0 = rbeg; r0 < rend; r0 += SCAN_RT) {
-        const long wr0 = r0 + wave * SCAN_WR;
-        f32x4 acc0[NG], acc1[NG];
+    const int n_it = rend > rbeg ? (int)((rend - rbeg + RWG - 1) / RWG) : 0;
+    const int nks = A.nks, nksp = A.nksp;
+    const size_t rowb = (size_t)A.d * ESZ;
+
+    float *nx = nx_all + wave * 2 * RW;
+    uint32_t *lk = lk_all + wave * BM * k;
+    int32_t *li = li_all + wave * BM * k;
+    int *lc = lc_all + wave * BM;
+    uint32_t *lmk = lmk_all + wave * BM;
+    int32_t *lmi = lmi_all + wave * BM;
+    int *sq = sq_all + wave * STAGE_CAP;
+    uint32_t *sk = sk_all + wave * STAGE_CAP;
+    int32_t *si = si_all + wave * STAGE_CAP;
+
+    for (int i = tid; i < BM; i += SCAN_THREADS) {
+        const int q = q0 + i;
+        qn_s[i] = q < A.B ? A.qn[q] : 0.f;
+        gb_s[i] = q < A.B ? A.tau[q] : 0u;
+    }
+    for (int i = tid; i < SCAN_WAVES * BM; i += SCAN_THREADS)
+        lc_all[i] = 0;
+
+    // ---- loads of one k-step, always issued, masked by select. The query
+    // items run two k-steps ahead of the MFMAs, the bank rows three.
+    int pq_it = 0, pq_s = 0;   // k-step of the next query load
+    int pb_it = 0, pb_s = 0;   // k-step of the next bank load
+    auto issue_q = [&](i32x4(&qs)[QPT]) {
+        const bool kv = pq_it < n_it && pq_s < nks;
+        const int kq = pq_s * KS;
+        const i32x4 z = {0, 0, 0, 0};
 #pragma unroll
-        for (int g = 0; g < NG; ++g) {
-            acc0[g] = f32x4{0.f, 0.f, 0.f, 0.f};
-            acc1[g] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int i = 0; i < QPT; ++i) {
+            const int item = tid + SCAN_THREADS * i;
+            const int f = item >> 6, l = item & 63;
+            const int q = q0 + f * 16 + (l & 15);
+            const int kk = kq + (l >> 4) * VEC;
+            const bool v = item < QITEMS && kv && q < A.B && kk < A.d;
+            const i32x4 x = load16(A.queries + (v ? (size_t)q * rowb + (size_t)kk * ESZ : 0));
+            qs[i] = v ? x : z;
         }
-        if (wr0 < rend) {
-            // A fragments: lane l holds bank row wr0 (+16) + l%16, the 16 bytes
-            // at (l/16)*16 of each 64-byte k-step.
-            const long ra = wr0 + col, rb = wr0 + 16 + col;
-            const bool va = ra < rend, vb = rb < rend;
-            const uint8_t *pa = A.bank + (size_t)(va ? ra : 0) * row_bytes + jgrp * 16;
-            const uint8_t *pb = A.bank + (size_t)(vb ? rb : 0) * row_bytes + jgrp * 16;
-            for (int s0 = 0; s0 < nks; s0 += KB) {
-                i32x4 xa[KB], xb[KB];
-#pragma unroll
-                for (int u = 0; u < KB; ++u) {
-                    const int s = s0 + u;
-                    const bool kv = s < nks && s * 4 * VEC + jgrp * VEC < A.d;
-                    const i32x4 z = {0, 0, 0, 0};
-                    xa[u] = (va && kv) ? *(const i32x4 *)(pa + (size_t)s * 64) : z;
-                    xb[u] = (vb && kv) ? *(const i32x4 *)(pb + (size_t)s * 64) : z;
-                }
-#pragma unroll
-                for (int u = 0; u < KB; ++u) {
-                    if (s0 + u < nks) {
-#pragma unroll
-                        for (int g = 0; g < NG; ++g) {
-                            const i32x4 bq = qfrag[((s0 + u) * NG + g) * WAVE + lane];
-                            mfma_step<DT>(xa[u], bq, acc0[g]);
-                            mfma_step<DT>(xb[u], bq, acc1[g]);
-                        }
-                    }
-                }
-            }
+        if (++pq_s == nksp) {
+            pq_s = 0;
+            ++pq_it;
         }
-        // Accumulator layout: lane l, element e is bank row 4*(l/16)+e of the
-        // 16-row tile against query 16g + l%16. Distance |q|^2 + |x|^2 - 2<q,x>.
+    };
+    auto issue_b = [&](i32x4(&a)[RT]) {
+        const bool kv = pb_it < n_it && pb_s < nks;
+        const i32x4 z = {0, 0, 0, 0};
+        const long wr0 = rbeg + (long)pb_it * RWG + wave * RW;
+        const int kk = pb_s * KS + jg * VEC;
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            const int rl = wave * SCAN_WR + h * 16 + jgrp * 4;
-            float xn[4];
-            bool rv[4];
+        for (int tt = 0; tt < RT; ++tt) {
+            const long row = wr0 + tt * 16 + col;
+            const bool v = kv && row < rend && kk < A.d;
+            const i32x4 x = load16(A.bank + (v ? (size_t)row * rowb + (size_t)kk * ESZ : 0));
+            a[tt] = v ? x : z;
+        }
+        if (++pb_s == nksp) {
+            pb_s = 0;
+            ++pb_it;
+        }
+    };
+    auto stage_queries = [&](int slot, const i32x4(&qs)[QPT]) {
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const long row = r0 + rl + e;
-                rv[e] = row < rend;
-                xn[e] = rv[e] ? A.bank_norms[row] : 0.f;
+        for (int i = 0; i < QPT; ++i) {
+            const int item = tid + SCAN_THREADS * i;
+            if (item < QITEMS)
+                qbuf[slot * QITEMS + item] = qs[i];
+        }
+    };
+    // -|x|^2/2 of bank row `lane` of this wave in iteration it (-inf past the chunk)
+    auto load_norm = [&](int it) -> float {
+        const long row = rbeg + (long)it * RWG + wave * RW + lane;
+        const bool v = it < n_it && row < rend;
+        const float xn = A.bank_norms[v ? row : 0];
+        return v ? -0.5f * xn : -INFINITY;
+    };
+    // Filter threshold of tile query i: a value is a candidate if acc >= nu (a
+    // superset of distance <= the query's bound; the exact test follows on
+    // insertion).
+    auto nu_of = [&](int i) -> float {
+        if (q0 + i >= A.B)
+            return INFINITY;
+        uint32_t tk = lds_load_relaxed(gb_s + i);
+        if (lc[i] == k)
+            tk = min(tk, lmk[i]);
+        if (tk == KEY_NONE)
+            return -FLT_MAX;
+        const float qq = qn_s[i], th = key2f(tk);
+        const float v = 0.5f * (qq - th);
+        return v - ldexpf(fabsf(qq) + fabsf(th) + fabsf(v), -21);
+    };
+    auto recompute_max = [&](int i) {
+        const uint64_t v = lane < k ? pack(lk[i * k + lane], li[i * k + lane]) : 0;
+        const uint64_t m = wave_max_u64(v);
+        if (lane == 0) {
+            lmk[i] = (uint32_t)(m >> 32);
+            lmi[i] = (int32_t)(uint32_t)m;
+            atomicMin(A.tau + q0 + i, (uint32_t)(m >> 32));
+        }
+    };
+    // Insert (key, idx) into this wave's list of tile query i (wave-uniform call).
+    auto insert = [&](int i, uint32_t key, int32_t idx) {
+        if (key > lds_load_relaxed(gb_s + i))
+            return;
+        const int n = lc[i];
+        if (n < k) {
+            if (lane == 0) {
+                lk[i * k + n] = key;
+                li[i * k + n] = idx;
+                lc[i] = n + 1;
             }
+            if (n + 1 == k)
+                recompute_max(i);
+            return;
+        }
+        const uint32_t mk = lmk[i];
+        const int32_t mi = lmi[i];
+        if (!(key < mk || (key == mk && idx < mi)))
+            return;
+        if (lane < k && lk[i * k + lane] == mk && li[i * k + lane] == mi) {
+            lk[i * k + lane] = key;
+            li[i * k + lane] = idx;
+        }
+        recompute_max(i);
+    };
+    auto flush = [&](int n) {
+        for (int s = 0; s < n; ++s) {
+            const int i = __builtin_amdgcn_readfirstlane(sq[s]);
+            const uint32_t key = (uint32_t)__builtin_amdgcn_readfirstlane((int)sk[s]);
+            const int32_t idx = __builtin_amdgcn_readfirstlane(si[s]);
+            insert(i, key, idx);
+        }
+    };
+
+    f32x4 acc[RT][NG];
+    i32x4 ring[R][RT];
+    i32x4 qst[2][QPT];
+    int x = 0;   // global k-step index of the MFMAs
+    const int total = n_it * nksp;
+
+    // One block of R k-steps.
+    auto block = [&]() {
+#pragma unroll
+        for (int u = 0; u < R; ++u) {
+            if (x > 0)
+                lds_barrier();
+            if (x + 1 < total)
+                stage_queries((u + 1) & 1, qst[(u + 1) & 1]);
+            issue_q(qst[u & 1]);
+            issue_b(ring[(u + P) % R]);
+            const i32x4 *qb = qbuf + (u & 1) * QITEMS;
 #pragma unroll
             for (int g = 0; g < NG; ++g) {
-                const int q = g * 16 + col;
-                const float qq = qn[q];
-                const f32x4 ac = h ? acc1[g] : acc0[g];
-                i32x4 w;
+                const i32x4 b = qb[g * WAVE + lane];
 #pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    w[e] = rv[e] ? (int)f2key(fmaf(-2.f, ac[e], qq + xn[e])) : (int)KEY_NONE;
-                *(i32x4 *)(dtile + q * SCAN_DSTRIDE + rl) = w;
+                for (int tt = 0; tt < RT; ++tt)
+                    acc[tt][g] = mfma_step<DT>(ring[u][tt], b, acc[tt][g]);
             }
+            ++x;
         }
-        __syncthreads();
+    };
 
-        // Selection: wave w owns queries w, w+4, ... A row survives if it beats
-        // this chunk's current k-th (strictly: every listed row has a lower
-        // index) and does not exceed the bound shared by all chunks (any
-        // chunk's k-th smallest distance bounds the global k-th from above).
-        for (int q = wave; q < QT; q += SCAN_WAVES) {
-            if (q0 + q >= A.B)
-                break;
-            const uint32_t k0 = dtile[q * SCAN_DSTRIDE + lane];
-            const uint32_t k1 = dtile[q * SCAN_DSTRIDE + WAVE + lane];
-            const int32_t i0 = (int32_t)(r0 + lane), i1 = (int32_t)(r0 + WAVE + lane);
-            const uint32_t lt = ltau[q];
-            const uint32_t gt = __hip_atomic_load(A.tau + q0 + q, __ATOMIC_RELAXED,
-                                                  __HIP_MEMORY_SCOPE_AGENT);
-            const bool p0 = k0 < lt && k0 <= gt;
-            const bool p1 = k1 < lt && k1 <= gt;
-            const uint64_t m0 = ballot(p0), m1 = ballot(p1);
-            if ((m0 | m1) == 0)
-                continue;
-            uint32_t *qk = lkey + q * k;
-            int32_t *qi = lidx + q * k;
-            const int cnt = lcnt[q];
-            const bool pl = lane < cnt;
-            const uint32_t kl = pl ? qk[lane] : KEY_NONE;
-            const int32_t il = pl ? qi[lane] : IDX_NONE;
-            const int n0 = popc(m0), n1 = popc(m1);
-            const int total = cnt + n0 + n1;
-            if (total < k) {
-                if (p0) {
-                    const int pos = cnt + mbcnt(m0);
-                    qk[pos] = k0;
-                    qi[pos] = i0;
+    // ---- pipeline prologue
+#pragma unroll
+    for (int u = 0; u < P; ++u)
+        issue_b(ring[u]);
+    issue_q(qst[0]);
+    issue_q(qst[1]);
+    stage_queries(0, qst[0]);
+    nx[lane] = load_norm(0);
+    float nx_next = load_norm(1);
+    lds_barrier();
+
+    for (int it = 0; it < n_it; ++it) {
+        // the accumulators start from -|x|^2/2 of their rows
+#pragma unroll
+        for (int tt = 0; tt < RT; ++tt) {
+            const f32x4 nxh = *(const f32x4 *)(nx + (it & 1) * RW + tt * 16 + jg * 4);
+#pragma unroll
+            for (int g = 0; g < NG; ++g)
+                acc[tt][g] = nxh;
+        }
+        for (int s0 = 0; s0 < nksp; s0 += R)
+            block();
+
+        // ---- end of iteration `it`: acc = -|x|^2/2 + <q, x>; dist = |q|^2 - 2*acc
+        nx[((it + 1) & 1) * RW + lane] = nx_next;
+        nx_next = load_norm(it + 2);
+        uint64_t any = 0;
+        static_for<0, NG>([&](auto G) {
+            constexpr int g = decltype(G)::value;
+            float m = -INFINITY;
+            static_for<0, RT>([&](auto TT) {
+                constexpr int tt = decltype(TT)::value;
+                m = fmaxf(m, fmaxf(fmaxf(acc[tt][g][0], acc[tt][g][1]),
+                                   fmaxf(acc[tt][g][2], acc[tt][g][3])));
+            });
+            any |= ballot(m >= nu_of(g * 16 + col));
+        });
+        if (any) {
+            const long wr0 = rbeg + (long)it * RWG + wave * RW;
+            // Stage the candidates of one (query group, row tile) in LDS; the
+            // switch keeps every accumulator access at a compile-time index.
+            auto stage = [&](auto G, auto TT) -> int {
+                constexpr int g = decltype(G)::value, tt = decltype(TT)::value;
+                const int i = g * 16 + col;
+                const float nu = nu_of(i);
+                const f32x4 a4 = acc[tt][g];
+                if (!ballot(fmaxf(fmaxf(a4[0], a4[1]), fmaxf(a4[2], a4[3])) >= nu))
+                    return 0;
+                const float qq = qn_s[i];
+                int nst = 0;
+                static_for<0, 4>([&](auto E) {
+                    constexpr int e = decltype(E)::value;
+                    const bool cnd = a4[e] >= nu;
+                    const uint64_t m = ballot(cnd);
+                    if (cnd) {
+                        const int pos = nst + mbcnt(m);
+                        sq[pos] = i;
+                        sk[pos] = f2key(fmaf(-2.f, a4[e], qq));
+                        si[pos] = (int32_t)(wr0 + tt * 16 + jg * 4 + e);
+                    }
+                    nst += popc(m);
+                });
+                return nst;
+            };
+            for (int gt = 0; gt < NG * RT; ++gt) {
+                int nst = 0;
+                switch (gt) {
+#define RB_STAGE_CASE(GT)                                                                          \
+    case GT:                                                                                       \
+        if constexpr (GT < NG * RT)                                                                \
+            nst = stage(Int<GT / RT>{}, Int<GT % RT>{});                                           \
+        break;
+                    RB_STAGE_CASE(0) RB_STAGE_CASE(1) RB_STAGE_CASE(2) RB_STAGE_CASE(3)
+                    RB_STAGE_CASE(4) RB_STAGE_CASE(5) RB_STAGE_CASE(6) RB_STAGE_CASE(7)
+                    RB_STAGE_CASE(8) RB_STAGE_CASE(9) RB_STAGE_CASE(10) RB_STAGE_CASE(11)
+                    RB_STAGE_CASE(12) RB_STAGE_CASE(13) RB_STAGE_CASE(14) RB_STAGE_CASE(15)
+                    RB_STAGE_CASE(16) RB_STAGE_CASE(17) RB_STAGE_CASE(18) RB_STAGE_CASE(19)
+                    RB_STAGE_CASE(20) RB_STAGE_CASE(21) RB_STAGE_CASE(22) RB_STAGE_CASE(23)
+                    RB_STAGE_CASE(24) RB_STAGE_CASE(25) RB_STAGE_CASE(26) RB_STAGE_CASE(27)
+                    RB_STAGE_CASE(28) RB_STAGE_CASE(29) RB_STAGE_CASE(30) RB_STAGE_CASE(31)
+                    RB_STAGE_CASE(32) RB_STAGE_CASE(33) RB_STAGE_CASE(34) RB_STAGE_CASE(35)
+                    RB_STAGE_CASE(36) RB_STAGE_CASE(37) RB_STAGE_CASE(38) RB_STAGE_CASE(39)
+                    RB_STAGE_CASE(40) RB_STAGE_CASE(41) RB_STAGE_CASE(42) RB_STAGE_CASE(43)
+                    RB_STAGE_CASE(44) RB_STAGE_CASE(45) RB_STAGE_CASE(46) RB_STAGE_CASE(47)
+                    RB_STAGE_CASE(48) RB_STAGE_CASE(49) RB_STAGE_CASE(50) RB_STAGE_CASE(51)
+                    RB_STAGE_CASE(52) RB_STAGE_CASE(53) RB_STAGE_CASE(54) RB_STAGE_CASE(55)
+                    RB_STAGE_CASE(56) RB_STAGE_CASE(57) RB_STAGE_CASE(58) RB_STAGE_CASE(59)
+                    RB_STAGE_CASE(60) RB_STAGE_CASE(61) RB_STAGE_CASE(62) RB_STAGE_CASE(63)
+#undef RB_STAGE_CASE
                 }
-                if (p1) {
-                    const int pos = cnt + n0 + mbcnt(m1);
-                    qk[pos] = k1;
-                    qi[pos] = i1;
-                }
-                if (lane == 0)
-                    lcnt[q] = total;
-                continue;
-            }
-            uint32_t T;
-            int32_t U;
-            select_k(kl, il, pl, k0, i0, p0, k1, i1, p1, k, T, U);
-            const bool sl = pl && (kl < T || (kl == T && il <= U));
-            const bool s0 = p0 && (k0 < T || (k0 == T && i0 <= U));
-            const bool s1 = p1 && (k1 < T || (k1 == T && i1 <= U));
-            const uint64_t ml = ballot(sl), ms0 = ballot(s0), ms1 = ballot(s1);
-            // the old list is in registers; rewrite the k kept entries compactly
-            if (sl) {
-                const int pos = mbcnt(ml);
-                qk[pos] = kl;
-                qi[pos] = il;
-            }
-            if (s0) {
-                const int pos = popc(ml) + mbcnt(ms0);
-                qk[pos] = k0;
-                qi[pos] = i0;
-            }
-            if (s1) {
-                const int pos = popc(ml) + popc(ms0) + mbcnt(ms1);
-                qk[pos] = k1;
-                qi[pos] = i1;
-            }
-            if (lane == 0) {
-                lcnt[q] = k;
-                ltau[q] = T;
-                if (T < gt)
-                    atomicMin(A.tau + q0 + q, T);
+                if (nst)
+                    flush(nst);
             }
         }
-        __syncthreads();
+        // pick up bounds other workgroups have lowered
+        for (int i = tid; i < BM; i += SCAN_THREADS)
+            if (q0 + i < A.B)
+                lds_store_relaxed(gb_s + i, __hip_atomic_load(A.tau + q0 + i, __ATOMIC_RELAXED,
+                                                              __HIP_MEMORY_SCOPE_AGENT));
     }
 
-    // This chunk's lists (unsorted, padded) -> workspace [B][n_chunks][k].
-    for (int q = wave; q < QT; q += SCAN_WAVES) {
-        if (q0 + q >= A.B)
+    // ---- this wave's lists -> workspace [B][W][k]
+    const int wl = c * SCAN_WAVES + wave;
+    for (int i = 0; i < BM; ++i) {
+        const int q = q0 + i;
+        if (q >= A.B)
             break;
-        const int cnt = lcnt[q];
-        for (int j = lane; j < k; j += WAVE) {
-            const size_t o = ((size_t)(q0 + q) * A.n_chunks + c) * k + j;
-            A.pkey[o] = j < cnt ? lkey[q * k + j] : KEY_NONE;
-            A.pidx[o] = j < cnt ? lidx[q * k + j] : IDX_NONE;
+        const int n = lc[i];
+        const size_t o = (size_t)q * A.W + wl;
+        if (lane == 0)
+            A.ccnt[o] = n;
+        if (lane < n) {
+            A.ckey[o * k + lane] = lk[i * k + lane];
+            A.cidx[o * k + lane] = li[i * k + lane];
         }
     }
 }
 
+// ------------------------------------------------------------------ merge
+
 struct MergeArgs {
-    const uint32_t *pkey;
-    const int32_t *pidx;
-    const uint32_t *tau;
-    int n_chunks, k;
+    const int32_t *ccnt;
+    const uint32_t *ckey;
+    const int32_t *cidx;
+    int W, B, k;
     int32_t *nbr_idx;
     float *nbr_dist;
     const float *qual, *len;
     int N, M;
     float *q_hat, *l_hat;
 };
-
-// Block-wide count: one barrier per call (two alternating slots).
-__device__ __forceinline__ int block_count(int c, int *red, int &phase)
-{
-    const float s = wave_sum((float)c);
-    int *slot = red + (phase & 1) * 4;
-    if (lane_id() == 0)
-        slot[threadIdx.x >> 6] = (int)s;
-    __syncthreads();
-    ++phase;
-    return slot[0] + slot[1] + slot[2] + slot[3];
-}
 
 // The label gather and average: sum over neighbours j = 0..k-1 in order. A
 // neighbour index outside [0, N) makes both averages NaN instead of reading
@@ -406,100 +652,128 @@ __device__ __forceinline__ void average_labels(const int32_t *nbr, int k, const 
     *l_out = sl / (float)k;
 }
 
-template <int EPT, bool PREDICT>
-__global__ __launch_bounds__(MERGE_THREADS) void merge_kernel(const MergeArgs A)
+// One wave per query: gather the lists' entries (into LDS when they fit),
+// select the k smallest (key, index) pairs bit by bit from the most
+// significant key bit, order them, then gather and average the labels.
+template <bool PREDICT>
+__global__ __launch_bounds__(MERGE_WAVES * WAVE) void merge_kernel(const MergeArgs A)
 {
-    __shared__ int red[8];
-    __shared__ uint32_t skey[RB_MAX_K_DEV];
-    __shared__ int32_t sidx[RB_MAX_K_DEV];
-    __shared__ int32_t sorted_idx[RB_MAX_K_DEV];
-    __shared__ int scount;
-    const int b = blockIdx.x, tid = threadIdx.x, k = A.k;
-    const int E = A.n_chunks * k;
-    const uint32_t *pk = A.pkey + (size_t)b * E;
-    const int32_t *pi = A.pidx + (size_t)b * E;
-    const uint32_t bound = A.tau[b];
-    uint32_t key[EPT];
-    int32_t idx[EPT];
-#pragma unroll
-    for (int e = 0; e < EPT; ++e) {
-        const int j = e * MERGE_THREADS + tid;
-        key[e] = KEY_NONE;
-        idx[e] = IDX_NONE;
-        if (j < E) {
-            const uint32_t kk = pk[j];
-            if (kk <= bound) {   // rows above the final bound cannot be among the k nearest
-                key[e] = kk;
-                idx[e] = pi[j];
+    __shared__ uint32_t ek_all[MERGE_WAVES][MERGE_CAP];
+    __shared__ int32_t ei_all[MERGE_WAVES][MERGE_CAP];
+    __shared__ uint32_t sk_all[MERGE_WAVES][RB_MAX_K_DEV];
+    __shared__ int32_t si_all[MERGE_WAVES][RB_MAX_K_DEV];
+    __shared__ int32_t so_all[MERGE_WAVES][RB_MAX_K_DEV];
+    const int wave = threadIdx.x >> 6, lane = lane_id();
+    const int b = blockIdx.x * MERGE_WAVES + wave;
+    if (b >= A.B)
+        return;
+    const int k = A.k, W = A.W;
+    uint32_t *ek = ek_all[wave];
+    int32_t *ei = ei_all[wave];
+    const int32_t *cnt = A.ccnt + (size_t)b * W;
+    const size_t base = (size_t)b * W * k;
+
+    // gather into LDS (entries past MERGE_CAP stay in global memory)
+    int total = 0;
+    for (int w0 = 0; w0 < W; w0 += WAVE) {
+        const int w = w0 + lane;
+        const int n = w < W ? cnt[w] : 0;
+        const int incl = wave_incl_scan(n);
+        const int off = total + incl - n;
+        for (int j = 0; j < n; ++j) {
+            if (off + j < MERGE_CAP) {
+                ek[off + j] = A.ckey[base + (size_t)w * k + j];
+                ei[off + j] = A.cidx[base + (size_t)w * k + j];
             }
         }
+        total += __shfl(incl, WAVE - 1);
     }
-    if (tid == 0)
-        scount = 0;
-    if (tid < k)
-        sorted_idx[tid] = IDX_NONE;
-    int phase = 0;
-    // T = k-th smallest key
+    const bool in_lds = total <= MERGE_CAP;
+    // entry e of the gathered sequence: (key, idx)
+    auto count_if = [&](auto pred) -> int {
+        int c = 0;
+        if (in_lds) {
+            for (int e = lane; e < total; e += WAVE)
+                c += pred(ek[e], ei[e]);
+        } else {
+            for (int w = 0; w < W; ++w) {
+                const int n = cnt[w];
+                if (lane < n)
+                    c += pred(A.ckey[base + (size_t)w * k + lane], A.cidx[base + (size_t)w * k + lane]);
+            }
+        }
+        return wave_sum_int(c);
+    };
     uint32_t prefix = 0;
     for (int bit = 31; bit >= 0; --bit) {
         const uint32_t trial = prefix | (1u << bit);
-        int c = 0;
-#pragma unroll
-        for (int e = 0; e < EPT; ++e)
-            c += (idx[e] != IDX_NONE && key[e] < trial);
-        if (block_count(c, red, phase) < k)
+        if (count_if([&](uint32_t kk, int32_t) { return kk < trial; }) < k)
             prefix = trial;
     }
     const uint32_t T = prefix;
-    int c_lt = 0, c_eq = 0;
-#pragma unroll
-    for (int e = 0; e < EPT; ++e) {
-        c_lt += (idx[e] != IDX_NONE && key[e] < T);
-        c_eq += (idx[e] != IDX_NONE && key[e] == T);
-    }
-    c_lt = block_count(c_lt, red, phase);
-    c_eq = block_count(c_eq, red, phase);
+    const int c_lt = count_if([&](uint32_t kk, int32_t) { return kk < T; });
+    const int c_eq = count_if([&](uint32_t kk, int32_t) { return kk == T; });
     const int r = k - c_lt;
     int32_t U = IDX_NONE;
     if (c_eq > r) {
         uint32_t up = 0;
         for (int bit = 30; bit >= 0; --bit) {
             const uint32_t trial = up | (1u << bit);
-            int c = 0;
-#pragma unroll
-            for (int e = 0; e < EPT; ++e)
-                c += (idx[e] != IDX_NONE && key[e] == T && (uint32_t)idx[e] < trial);
-            if (block_count(c, red, phase) < r)
+            if (count_if([&](uint32_t kk, int32_t ii) { return kk == T && (uint32_t)ii < trial; }) < r)
                 up = trial;
         }
         U = (int32_t)up;
     }
-#pragma unroll
-    for (int e = 0; e < EPT; ++e) {
-        if (idx[e] != IDX_NONE && (key[e] < T || (key[e] == T && idx[e] <= U))) {
-            const int pos = atomicAdd(&scount, 1);
-            skey[pos] = key[e];
-            sidx[pos] = idx[e];
+    // the k selected entries, compacted
+    uint32_t *sk = sk_all[wave];
+    int32_t *si = si_all[wave];
+    int32_t *so = so_all[wave];
+    if (lane < k) {
+        sk[lane] = KEY_NONE;
+        si[lane] = IDX_NONE;
+        so[lane] = IDX_NONE;
+    }
+    int ns = 0;
+    auto take = [&](uint32_t kk, int32_t ii, bool valid) {
+        const bool s = valid && (kk < T || (kk == T && ii <= U));
+        const uint64_t m = ballot(s);
+        if (s) {
+            const int pos = ns + mbcnt(m);
+            if (pos < k) {
+                sk[pos] = kk;
+                si[pos] = ii;
+            }
+        }
+        ns += popc(m);
+    };
+    if (in_lds) {
+        for (int e0 = 0; e0 < total; e0 += WAVE) {
+            const int e = e0 + lane;
+            take(e < total ? ek[e] : KEY_NONE, e < total ? ei[e] : IDX_NONE, e < total);
+        }
+    } else {
+        for (int w = 0; w < W; ++w) {
+            const int n = cnt[w];
+            take(lane < n ? A.ckey[base + (size_t)w * k + lane] : KEY_NONE,
+                 lane < n ? A.cidx[base + (size_t)w * k + lane] : IDX_NONE, lane < n);
         }
     }
-    __syncthreads();
-    // exactly k entries; order them by (key, index)
-    if (tid < k) {
-        const uint32_t mk = skey[tid];
-        const int32_t mi = sidx[tid];
+    // order by (key, index)
+    if (lane < k) {
+        const uint32_t mk = sk[lane];
+        const int32_t mi = si[lane];
         int rank = 0;
         for (int j = 0; j < k; ++j)
-            rank += (skey[j] < mk || (skey[j] == mk && sidx[j] < mi));
+            rank += (sk[j] < mk || (sk[j] == mk && si[j] < mi));
         A.nbr_idx[(size_t)b * k + rank] = mi;
         if (A.nbr_dist)
             A.nbr_dist[(size_t)b * k + rank] = key2f(mk);
-        sorted_idx[rank] = mi;
+        so[rank] = mi;
     }
     if constexpr (PREDICT) {
-        __syncthreads();
-        for (int m = tid; m < A.M; m += MERGE_THREADS)
-            average_labels(sorted_idx, k, A.qual, A.len, A.N, A.M, m,
-                           A.q_hat + (size_t)b * A.M + m, A.l_hat + (size_t)b * A.M + m);
+        for (int m = lane; m < A.M; m += WAVE)
+            average_labels(so, k, A.qual, A.len, A.N, A.M, m, A.q_hat + (size_t)b * A.M + m,
+                           A.l_hat + (size_t)b * A.M + m);
     }
 }
 
@@ -519,33 +793,62 @@ __global__ __launch_bounds__(64) void predict_kernel(const int32_t *__restrict__
                        l_hat + (size_t)b * M + m);
 }
 
-template <int DT, int NG>
-hipError_t launch_scan(const ScanArgs &a, size_t lds, int grid, hipStream_t s)
-{
-    hipError_t e = hipFuncSetAttribute((const void *)scan_kernel<DT, NG>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess)
-        return e;
-    hipLaunchKernelGGL((scan_kernel<DT, NG>), dim3(grid), dim3(SCAN_THREADS), lds, s, a);
-    return hipGetLastError();
-}
-
-template <bool PRED>
-hipError_t launch_merge(const MergeArgs &a, int B, int ept, hipStream_t s)
-{
-    switch (ept) {
-    case 4: hipLaunchKernelGGL((merge_kernel<4, PRED>), dim3(B), dim3(MERGE_THREADS), 0, s, a); break;
-    case 8: hipLaunchKernelGGL((merge_kernel<8, PRED>), dim3(B), dim3(MERGE_THREADS), 0, s, a); break;
-    case 16: hipLaunchKernelGGL((merge_kernel<16, PRED>), dim3(B), dim3(MERGE_THREADS), 0, s, a); break;
-    case 32: hipLaunchKernelGGL((merge_kernel<32, PRED>), dim3(B), dim3(MERGE_THREADS), 0, s, a); break;
-    default: return hipErrorInvalidValue;
-    }
-    return hipGetLastError();
-}
+// ------------------------------------------------------------------ host side
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+size_t scan_lds_bytes(int ng, int k)
+{
+    const size_t bm = (size_t)ng * 16;
+    return 2 * (size_t)ng * WAVE * 16 +   // query double buffer: 2 x ng fragments of 1 KB
+           bm * 8 +                       // |q|^2, bound snapshot
+           (size_t)SCAN_WAVES * 2 * SCAN_RT * 16 * 4 +   // bank norms of two iterations
+           (size_t)SCAN_WAVES * bm * k * 8 +   // lists
+           (size_t)SCAN_WAVES * bm * 12 +      // counts, max key, max index
+           (size_t)SCAN_WAVES * STAGE_CAP * 12;
+}
+
 thread_local hipEvent_t t_scan_begin = nullptr, t_scan_end = nullptr;
+
+template <int DT, int NG, int RT>
+hipError_t launch_scan(const ScanArgs &a, size_t lds, int grid, hipStream_t s)
+{
+    hipError_t e = hipFuncSetAttribute((const void *)scan_kernel<DT, NG, RT>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess)
+        return e;
+    hipLaunchKernelGGL((scan_kernel<DT, NG, RT>), dim3(grid), dim3(SCAN_THREADS), lds, s, a);
+    return hipGetLastError();
+}
+
+template <int DT>
+hipError_t launch_scan_dt(const KnnPlan &p, const ScanArgs &a, int grid, hipStream_t s)
+{
+    switch (p.ng) {
+    case 16: return launch_scan<DT, 16, SCAN_RT>(a, p.lds_bytes, grid, s);
+    case 8: return launch_scan<DT, 8, SCAN_RT>(a, p.lds_bytes, grid, s);
+    case 4: return launch_scan<DT, 4, SCAN_RT>(a, p.lds_bytes, grid, s);
+    case 2: return launch_scan<DT, 2, SCAN_RT>(a, p.lds_bytes, grid, s);
+    case 1: return launch_scan<DT, 1, SCAN_RT>(a, p.lds_bytes, grid, s);
+    }
+    return hipErrorInvalidValue;
+}
+
+template <int DT>
+hipError_t launch_seed_bound(const KnnPlan &p, const void *queries, const float *gmin, float *qn,
+                             uint32_t *tau, hipStream_t s)
+{
+    const int grid = (p.B + 3) / 4;
+    const uint8_t *q = (const uint8_t *)queries;
+    const int G = p.S ? p.G : 0;
+    if (G <= 1024)
+        hipLaunchKernelGGL((seed_bound_kernel<DT, 16>), dim3(grid), dim3(256), 0, s, q, p.B, p.d,
+                           p.k, gmin, G, qn, tau);
+    else
+        hipLaunchKernelGGL((seed_bound_kernel<DT, 32>), dim3(grid), dim3(256), 0, s, q, p.B, p.d,
+                           p.k, gmin, G, qn, tau);
+    return hipGetLastError();
+}
 
 }  // namespace
 
@@ -564,15 +867,14 @@ int plan_knn(int B, int N, int d, int dtype, int k, int num_cu, KnnPlan *p)
     p->d = d;
     p->k = k;
     p->nks = (d + 4 * vec - 1) / (4 * vec);
-    // largest query tile that is useful for B and fits in LDS
-    const int b16 = (B + 15) / 16;
+    p->nksp = (p->nks + SCAN_UNROLL - 1) / SCAN_UNROLL * SCAN_UNROLL;
+    // largest query tile that B can fill and that fits in LDS
+    int want = 1;
+    while (want < 16 && want * 16 < B)
+        want *= 2;
     p->ng = 0;
-    for (int ng = 4; ng >= 1; ng >>= 1) {
-        if (ng > 1 && ng > b16)
-            continue;
-        const int qt = ng * 16;
-        const size_t lds = (size_t)p->nks * ng * WAVE * 16 + (size_t)qt * 4 +
-                           (size_t)qt * SCAN_DSTRIDE * 4 + (size_t)qt * k * 8 + (size_t)qt * 8;
+    for (int ng = want; ng >= 1; ng /= 2) {
+        const size_t lds = scan_lds_bytes(ng, k);
         if (lds <= LDS_LIMIT) {
             p->ng = ng;
             p->lds_bytes = lds;
@@ -581,32 +883,47 @@ int plan_knn(int B, int N, int d, int dtype, int k, int num_cu, KnnPlan *p)
     }
     if (p->ng == 0)
         return -1;
-    const int qt = p->ng * 16;
-    p->n_qt = B > 0 ? (B + qt - 1) / qt : 1;
+    p->rt = SCAN_RT;
+    const int bm = p->ng * 16;
+    p->n_qt = B > 0 ? (B + bm - 1) / bm : 1;
     // one workgroup per compute unit (the LDS use allows no more)
-    int chunks = num_cu / p->n_qt;
+    long chunks = num_cu / p->n_qt;
     if (chunks < 1)
         chunks = 1;
-    const int max_by_merge = MERGE_MAX_ENTRIES / k;
-    if (chunks > max_by_merge)
-        chunks = max_by_merge;
-    const int max_by_rows = (N + 31) / 32;   // chunks of at least 32 rows
-    if (chunks > max_by_rows)
-        chunks = max_by_rows;
-    if (chunks < 1)
-        chunks = 1;
-    p->n_chunks = chunks;
-    p->rows_per_chunk = ((long)N + chunks - 1) / chunks;
+    const long max_chunks = ((long)N + 15) / 16;
+    if (chunks > max_chunks)
+        chunks = max_chunks;
+    long rpc = ((long)N + chunks - 1) / chunks;
+    rpc = (rpc + 15) / 16 * 16;
+    p->rows_per_chunk = rpc;
+    p->n_chunks = (int)(((long)N + rpc - 1) / rpc);
+    p->W = p->n_chunks * SCAN_WAVES;
+    // seed sample: about N/32 rows, 2048..32768, a multiple of 64 and at most N
+    long S = N / 32;
+    if (S < 2048)
+        S = 2048;
+    if (S > 32768)
+        S = 32768;
+    if (S > N)
+        S = N;
+    S = S / 64 * 64;
+    if (S / 16 < k)
+        S = 0;
+    p->S = (int)S;
+    p->G = (int)(S / 16);
     size_t off = 0;
     p->off_tau = off;
     off += align256((size_t)B * 4);
-    const size_t off_qn = off;
-    (void)off_qn;
+    p->off_qn = off;
     off += align256((size_t)B * 4);
-    p->off_pkey = off;
-    off += align256((size_t)B * chunks * k * 4);
-    p->off_pidx = off;
-    off += align256((size_t)B * chunks * k * 4);
+    p->off_gmin = off;
+    off += align256((size_t)B * (p->G > 0 ? p->G : 1) * 4);
+    p->off_ccnt = off;
+    off += align256((size_t)B * p->W * 4);
+    p->off_ckey = off;
+    off += align256((size_t)B * p->W * k * 4);
+    p->off_cidx = off;
+    off += align256((size_t)B * p->W * k * 4);
     p->bytes = off;
     return 0;
 }
@@ -634,18 +951,37 @@ hipError_t launch_knn(const KnnPlan &p, const void *queries, const void *bank,
 {
     uint8_t *w = (uint8_t *)ws;
     uint32_t *tau = (uint32_t *)(w + p.off_tau);
-    float *qn = (float *)(w + p.off_tau + align256((size_t)p.B * 4));
-    uint32_t *pkey = (uint32_t *)(w + p.off_pkey);
-    int32_t *pidx = (int32_t *)(w + p.off_pidx);
+    float *qn = (float *)(w + p.off_qn);
+    float *gmin = (float *)(w + p.off_gmin);
+    int32_t *ccnt = (int32_t *)(w + p.off_ccnt);
+    uint32_t *ckey = (uint32_t *)(w + p.off_ckey);
+    int32_t *cidx = (int32_t *)(w + p.off_cidx);
+    hipError_t e;
 
-    const int init_grid = (p.B + 3) / 4;
-    if (p.dtype == 1)
-        hipLaunchKernelGGL(knn_init_kernel<1>, dim3(init_grid), dim3(256), 0, s,
-                           (const uint8_t *)queries, p.B, p.d, qn, tau);
-    else
-        hipLaunchKernelGGL(knn_init_kernel<0>, dim3(init_grid), dim3(256), 0, s,
-                           (const uint8_t *)queries, p.B, p.d, qn, tau);
-    hipError_t e = hipGetLastError();
+    if (p.S > 0) {
+        SeedArgs sa;
+        sa.queries = (const uint8_t *)queries;
+        sa.bank = (const uint8_t *)bank;
+        sa.bank_norms = bank_norms;
+        sa.B = p.B;
+        sa.N = p.N;
+        sa.d = p.d;
+        sa.nks = p.nks;
+        sa.S = p.S;
+        sa.G = p.G;
+        sa.n_qg = (p.B + 15) / 16;
+        sa.gmin = gmin;
+        const long waves = (long)sa.n_qg * (p.S / 64);
+        const int grid = (int)((waves + 3) / 4);
+        if (p.dtype == 1)
+            hipLaunchKernelGGL(seed_groups_kernel<1>, dim3(grid), dim3(256), 0, s, sa);
+        else
+            hipLaunchKernelGGL(seed_groups_kernel<0>, dim3(grid), dim3(256), 0, s, sa);
+        if ((e = hipGetLastError()) != hipSuccess)
+            return e;
+    }
+    e = p.dtype == 1 ? launch_seed_bound<1>(p, queries, gmin, qn, tau, s)
+                     : launch_seed_bound<0>(p, queries, gmin, qn, tau, s);
     if (e != hipSuccess)
         return e;
 
@@ -659,35 +995,31 @@ hipError_t launch_knn(const KnnPlan &p, const void *queries, const void *bank,
     a.d = p.d;
     a.k = p.k;
     a.nks = p.nks;
+    a.nksp = p.nksp;
     a.n_chunks = p.n_chunks;
     a.n_qt = p.n_qt;
+    a.W = p.W;
     a.rows_per_chunk = p.rows_per_chunk;
     a.tau = tau;
-    a.pkey = pkey;
-    a.pidx = pidx;
+    a.ccnt = ccnt;
+    a.ckey = ckey;
+    a.cidx = cidx;
     const int grid = ((p.n_chunks + 7) / 8) * 8 * p.n_qt;
     const bool timed = t_scan_begin && t_scan_end;
     if (timed && (e = hipEventRecord(t_scan_begin, s)) != hipSuccess)
         return e;
-    if (p.dtype == 1) {
-        if (p.ng == 4) e = launch_scan<1, 4>(a, p.lds_bytes, grid, s);
-        else if (p.ng == 2) e = launch_scan<1, 2>(a, p.lds_bytes, grid, s);
-        else e = launch_scan<1, 1>(a, p.lds_bytes, grid, s);
-    } else {
-        if (p.ng == 4) e = launch_scan<0, 4>(a, p.lds_bytes, grid, s);
-        else if (p.ng == 2) e = launch_scan<0, 2>(a, p.lds_bytes, grid, s);
-        else e = launch_scan<0, 1>(a, p.lds_bytes, grid, s);
-    }
+    e = p.dtype == 1 ? launch_scan_dt<1>(p, a, grid, s) : launch_scan_dt<0>(p, a, grid, s);
     if (e != hipSuccess)
         return e;
     if (timed && (e = hipEventRecord(t_scan_end, s)) != hipSuccess)
         return e;
 
     MergeArgs m;
-    m.pkey = pkey;
-    m.pidx = pidx;
-    m.tau = tau;
-    m.n_chunks = p.n_chunks;
+    m.ccnt = ccnt;
+    m.ckey = ckey;
+    m.cidx = cidx;
+    m.W = p.W;
+    m.B = p.B;
     m.k = p.k;
     m.nbr_idx = nbr_idx;
     m.nbr_dist = nbr_dist;
@@ -697,13 +1029,12 @@ hipError_t launch_knn(const KnnPlan &p, const void *queries, const void *bank,
     m.M = M;
     m.q_hat = q_hat;
     m.l_hat = l_hat;
-    const int E = p.n_chunks * p.k;
-    int ept = 4;
-    while (ept * MERGE_THREADS < E)
-        ept *= 2;
-    if (ept > MERGE_MAX_EPT)
-        return hipErrorInvalidValue;
-    return q_hat ? launch_merge<true>(m, p.B, ept, s) : launch_merge<false>(m, p.B, ept, s);
+    const int mgrid = (p.B + MERGE_WAVES - 1) / MERGE_WAVES;
+    if (q_hat)
+        hipLaunchKernelGGL(merge_kernel<true>, dim3(mgrid), dim3(MERGE_WAVES * WAVE), 0, s, m);
+    else
+        hipLaunchKernelGGL(merge_kernel<false>, dim3(mgrid), dim3(MERGE_WAVES * WAVE), 0, s, m);
+    return hipGetLastError();
 }
 
 hipError_t launch_predict(const int32_t *nbr_idx, int B, int k, const float *bank_qual,
