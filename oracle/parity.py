@@ -7,7 +7,10 @@ Tolerances (floating point fixed at 1e-5 relative for decisions and 1e-4 for
 values):
   rel(a, b) = |a - b| / max(|a|, |b|, f), f = 1 for squared distances of
   unit-scale embeddings (fp32 cancellation in |q|^2 + |x|^2 - 2<q,x> is
-  absolute, about 1e-6 at d = 768), f = 1e-6 otherwise.
+  absolute, about 1e-6 at d = 768); f = 1e-2 for Eq. 1 scores, which are
+  unit-scale sums of terms in [0, 1] (1 - C/Cmax near the maximum loses all
+  relative precision in fp32, leaving ~1e-7 absolute error); f = 1e-6 for
+  predictions and state.
   * neighbours: an index in one list but not the other must sit within 1e-5 of
     the oracle's k-th distance (a boundary near-tie); order may differ only
     among near-equal distances; GPU distances of listed rows within 1e-5.
@@ -31,6 +34,7 @@ DIST_RTOL = 1e-5
 DIST_FLOOR = 1.0
 VAL_RTOL = 1e-4
 VAL_FLOOR = 1e-6
+SCORE_FLOOR = 1e-2
 PICK_RTOL = 1e-5
 
 
@@ -94,7 +98,7 @@ def check_predictions(g_idx, g_qhat, g_lhat, qual, length, label=""):
 
 def check_scores(g_S0, g_qhat, g_lhat, plen, inst, weights, label=""):
     S0 = _score(np.asarray(g_qhat, np.float64), np.asarray(g_lhat, np.float64), plen, inst, weights)
-    e = rel(g_S0, S0, VAL_FLOOR)
+    e = rel(g_S0, S0, SCORE_FLOOR)
     assert e.max() <= VAL_RTOL, f"{label} S0 rel err {e.max()} at {np.unravel_index(e.argmax(), e.shape)}"
     return float(e.max())
 
@@ -116,11 +120,11 @@ def check_assign(g_assign, g_chosen, g_qhat, g_lhat, plen, inst, weights, g_fina
         assert 0 <= ig < S.shape[0], f"{label} step {r}: pick {ig} out of range"
         if ig != io:
             gap = S[io] - S[ig]
-            assert gap <= PICK_RTOL * max(abs(S[io]), 1e-6), \
+            assert gap <= PICK_RTOL * max(abs(S[io]), SCORE_FLOOR), \
                 f"{label} step {r}: gpu picked {ig} (S={S[ig]}) oracle {io} (S={S[io]})"
             ties += 1
         if g_chosen is not None:
-            assert rel(g_chosen[r], S[ig], VAL_FLOOR) <= VAL_RTOL, \
+            assert rel(g_chosen[r], S[ig], SCORE_FLOOR) <= VAL_RTOL, \
                 f"{label} step {r}: chosen score {g_chosen[r]} vs {S[ig]}"
         p[ig] += plen[r]
         a[ig] += lh[r, model[ig]]

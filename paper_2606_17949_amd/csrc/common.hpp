@@ -47,22 +47,57 @@ __device__ __forceinline__ int lane_id() { return threadIdx.x & (WAVE - 1); }
 __device__ __forceinline__ float bf16lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
-// Wave-wide reductions through DPP row operations plus cross-row lane reads.
-// All lanes receive the result.
+// Wave-wide reductions: a butterfly inside each row of 16 lanes (quad
+// permutes, then half-row and row mirrors), then the row_bcast:15 and
+// row_bcast:31 steps carry rows 0..2 into row 3; lane 63 ends with the whole
+// wave's result, which is broadcast through a scalar register.
+template <typename T, typename F>
+__device__ __forceinline__ T wave_reduce(T v, F op)
+{
+    static_assert(sizeof(T) == 4, "32-bit values");
+    auto dpp = [](T x, int ctrl, int row_mask) -> T {
+        const int xi = __builtin_bit_cast(int, x);
+        int r;
+        switch (ctrl) {   // the control must be a compile-time constant
+        case 0xb1: r = __builtin_amdgcn_update_dpp(xi, xi, 0xb1, 0xf, 0xf, false); break;
+        case 0x4e: r = __builtin_amdgcn_update_dpp(xi, xi, 0x4e, 0xf, 0xf, false); break;
+        case 0x141: r = __builtin_amdgcn_update_dpp(xi, xi, 0x141, 0xf, 0xf, false); break;
+        case 0x140: r = __builtin_amdgcn_update_dpp(xi, xi, 0x140, 0xf, 0xf, false); break;
+        case 0x142: r = __builtin_amdgcn_update_dpp(xi, xi, 0x142, 0xa, 0xf, false); break;
+        default: r = __builtin_amdgcn_update_dpp(xi, xi, 0x143, 0xc, 0xf, false); break;
+        }
+        (void)row_mask;
+        return __builtin_bit_cast(T, r);
+    };
+    v = op(v, dpp(v, 0xb1, 0xf));    // quad_perm [1,0,3,2]
+    v = op(v, dpp(v, 0x4e, 0xf));    // quad_perm [2,3,0,1]
+    v = op(v, dpp(v, 0x141, 0xf));   // row_half_mirror
+    v = op(v, dpp(v, 0x140, 0xf));   // row_mirror: every lane holds its row's result
+    v = op(v, dpp(v, 0x142, 0xa));   // row_bcast:15 into rows 1 and 3
+    v = op(v, dpp(v, 0x143, 0xc));   // row_bcast:31 into rows 2 and 3
+    return __builtin_bit_cast(T, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
+}
+
 template <typename F>
 __device__ __forceinline__ float wave_reduce_f(float v, F op)
 {
-    // within each row of 16 lanes: xor 1, 2 via quad permutes; 4, 8 via mirrors
-    v = op(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xb1, 0xf, 0xf, false)));  // quad_perm [1,0,3,2]
-    v = op(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x4e, 0xf, 0xf, false)));  // quad_perm [2,3,0,1]
-    v = op(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x141, 0xf, 0xf, false))); // row_half_mirror
-    v = op(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x140, 0xf, 0xf, false))); // row_mirror
-    // across the four rows
-    float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
-    float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
-    float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
-    float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
-    return op(op(r0, r1), op(r2, r3));
+    return wave_reduce(v, op);
+}
+
+template <typename F>
+__device__ __forceinline__ uint32_t wave_reduce_u32(uint32_t v, F op)
+{
+    return wave_reduce(v, op);
+}
+
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v)
+{
+    return wave_reduce_u32(v, [](uint32_t a, uint32_t b) { return a > b ? a : b; });
+}
+
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t v)
+{
+    return wave_reduce_u32(v, [](uint32_t a, uint32_t b) { return a < b ? a : b; });
 }
 
 __device__ __forceinline__ float wave_max(float v)

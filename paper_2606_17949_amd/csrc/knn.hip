@@ -79,6 +79,21 @@ __device__ __forceinline__ f32x4 mfma_step(const i32x4 &a, const i32x4 &b, const
 
 __device__ __forceinline__ i32x4 load16(const uint8_t *p) { return *(const i32x4 *)p; }
 
+// Raw buffer resource over [base, base + bytes): loads at or past the end
+// return zero, which masks rows past a chunk and queries past the batch.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, uint32_t bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes,
+                                             0x00020000);
+}
+
+__device__ __forceinline__ i32x4 buffer_load16(__amdgpu_buffer_rsrc_t r, uint32_t voffset)
+{
+    return __builtin_bit_cast(i32x4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)voffset, 0, 0));
+}
+
+constexpr uint32_t OFF_NONE = 0x80000000u;   // a buffer offset past any resource
+
 template <int I> struct Int {
     static constexpr int value = I;
 };
@@ -188,15 +203,19 @@ __device__ __forceinline__ long seed_row(int j, int N, int S)
 }
 
 // One wave per (query group of 16, block of 64 sample rows): partial distances
-// p = |x|^2 - 2<q,x> by MFMA, then each lane's minimum over its 16 rows.
+// p = |x|^2 - 2<q,x> by MFMA, then each lane's minimum over its 16 rows. The
+// 16 waves of a workgroup take 16 query groups of the same sample block, so
+// the block's rows are fetched once into the compute unit's caches.
+constexpr int SEED_WAVES = 16;
+
 template <int DT>
-__global__ __launch_bounds__(256) void seed_groups_kernel(const SeedArgs A)
+__global__ __launch_bounds__(SEED_WAVES * WAVE) void seed_groups_kernel(const SeedArgs A)
 {
     constexpr int VEC = Elem<DT>::VEC, ESZ = Elem<DT>::ESZ;
     const int lane = lane_id(), col = lane & 15, jg = lane >> 4;
-    const int wid = (int)(((long)blockIdx.x * blockDim.x + threadIdx.x) >> 6);
-    const int qg = wid % A.n_qg, sb = wid / A.n_qg;
-    if (sb >= A.S / 64)
+    const int sb = blockIdx.x;
+    const int qg = blockIdx.y * SEED_WAVES + (threadIdx.x >> 6);
+    if (qg >= A.n_qg)
         return;
     const size_t rowb = (size_t)A.d * ESZ;
     const int q = qg * 16 + col;
@@ -265,7 +284,7 @@ __global__ __launch_bounds__(256) void seed_bound_kernel(const uint8_t *__restri
 #pragma unroll
             for (int u = 0; u < GPL; ++u)
                 c += key[u] < trial;
-            if (wave_sum_int(c) < k)
+            if ((int)wave_sum((float)c) < k)
                 prefix = trial;
         }
         const float pk = key2f(prefix);
@@ -292,7 +311,7 @@ struct ScanArgs {
     int32_t *cidx;    // [B][W][k]
 };
 
-template <int DT, int NG, int RT>
+template <int DT, int NG, int RT, bool RAGGED>
 __global__ __launch_bounds__(SCAN_THREADS, 1) void scan_kernel(const ScanArgs A)
 {
     constexpr int BM = NG * 16;
@@ -357,44 +376,53 @@ __global__ __launch_bounds__(SCAN_THREADS, 1) void scan_kernel(const ScanArgs A)
     for (int i = tid; i < SCAN_WAVES * BM; i += SCAN_THREADS)
         lc_all[i] = 0;
 
-    // ---- loads of one k-step, always issued, masked by select. The query
-    // items run two k-steps ahead of the MFMAs, the bank rows three.
-    int pq_it = 0, pq_s = 0;   // k-step of the next query load
-    int pb_it = 0, pb_s = 0;   // k-step of the next bank load
+    // ---- loads of one k-step through buffer resources whose base moves by one
+    // k-step (64 bytes of a row) per step; each lane keeps a fixed offset. Rows
+    // past the chunk and queries past the batch fall outside the resource and
+    // load zero; so does every lane of a padding k-step (empty resource). The
+    // query items run two k-steps ahead of the MFMAs, the bank rows three.
+    const uint8_t *bank_c = A.bank + (size_t)rbeg * rowb;
+    const uint32_t bank_c_bytes = (uint32_t)((rend - rbeg) * (long)rowb);
+    const uint32_t q_bytes = (uint32_t)((size_t)A.B * rowb);
+    uint32_t qvo[QPT];   // per item: q*rowb + (l/16)*16, or OFF_NONE
+    int qkk[QPT];        // element offset of the item within a k-step
+#pragma unroll
+    for (int i = 0; i < QPT; ++i) {
+        const int item = tid + SCAN_THREADS * i;
+        const int f = item >> 6, l = item & 63;
+        const int q = q0 + f * 16 + (l & 15);
+        qkk[i] = (l >> 4) * VEC;
+        qvo[i] = item < QITEMS ? (uint32_t)((size_t)q * rowb + (l >> 4) * 16) : OFF_NONE;
+    }
+    int pq_s = 0;             // k-step of the next query load (every iteration is the same)
+    int pb_it = 0, pb_s = 0;  // k-step of the next bank load
+    uint32_t bvo = (uint32_t)((size_t)(wave * RW + col) * rowb + jg * 16);   // tile 0 of pb_it
     auto issue_q = [&](i32x4(&qs)[QPT]) {
-        const bool kv = pq_it < n_it && pq_s < nks;
-        const int kq = pq_s * KS;
-        const i32x4 z = {0, 0, 0, 0};
+        const bool real = pq_s < nks;
+        const __amdgpu_buffer_rsrc_t r =
+            make_rsrc(A.queries + pq_s * KSTEP_BYTES, real ? q_bytes - pq_s * KSTEP_BYTES : 0u);
 #pragma unroll
         for (int i = 0; i < QPT; ++i) {
-            const int item = tid + SCAN_THREADS * i;
-            const int f = item >> 6, l = item & 63;
-            const int q = q0 + f * 16 + (l & 15);
-            const int kk = kq + (l >> 4) * VEC;
-            const bool v = item < QITEMS && kv && q < A.B && kk < A.d;
-            const i32x4 x = load16(A.queries + (v ? (size_t)q * rowb + (size_t)kk * ESZ : 0));
-            qs[i] = v ? x : z;
+            uint32_t vo = qvo[i];
+            if constexpr (RAGGED)
+                vo = pq_s * KS + qkk[i] < A.d ? vo : OFF_NONE;
+            qs[i] = buffer_load16(r, vo);
         }
-        if (++pq_s == nksp) {
+        if (++pq_s == nksp)
             pq_s = 0;
-            ++pq_it;
-        }
     };
     auto issue_b = [&](i32x4(&a)[RT]) {
-        const bool kv = pb_it < n_it && pb_s < nks;
-        const i32x4 z = {0, 0, 0, 0};
-        const long wr0 = rbeg + (long)pb_it * RWG + wave * RW;
-        const int kk = pb_s * KS + jg * VEC;
+        const bool real = pb_it < n_it && pb_s < nks;
+        const __amdgpu_buffer_rsrc_t r = make_rsrc(
+            bank_c + pb_s * KSTEP_BYTES, real ? bank_c_bytes - pb_s * KSTEP_BYTES : 0u);
+        const bool lane_ok = !RAGGED || pb_s * KS + jg * VEC < A.d;
 #pragma unroll
-        for (int tt = 0; tt < RT; ++tt) {
-            const long row = wr0 + tt * 16 + col;
-            const bool v = kv && row < rend && kk < A.d;
-            const i32x4 x = load16(A.bank + (v ? (size_t)row * rowb + (size_t)kk * ESZ : 0));
-            a[tt] = v ? x : z;
-        }
+        for (int tt = 0; tt < RT; ++tt)
+            a[tt] = buffer_load16(r, lane_ok ? bvo + (uint32_t)(tt * 16 * rowb) : OFF_NONE);
         if (++pb_s == nksp) {
             pb_s = 0;
             ++pb_it;
+            bvo += (uint32_t)(RWG * rowb);
         }
     };
     auto stage_queries = [&](int slot, const i32x4(&qs)[QPT]) {
@@ -487,12 +515,14 @@ __global__ __launch_bounds__(SCAN_THREADS, 1) void scan_kernel(const ScanArgs A)
             issue_q(qst[u & 1]);
             issue_b(ring[(u + P) % R]);
             const i32x4 *qb = qbuf + (u & 1) * QITEMS;
+            i32x4 b = qb[lane];
 #pragma unroll
             for (int g = 0; g < NG; ++g) {
-                const i32x4 b = qb[g * WAVE + lane];
+                const i32x4 bn = qb[((g + 1) % NG) * WAVE + lane];   // next fragment, in flight
 #pragma unroll
                 for (int tt = 0; tt < RT; ++tt)
                     acc[tt][g] = mfma_step<DT>(ring[u][tt], b, acc[tt][g]);
+                b = bn;
             }
             ++x;
         }
@@ -652,57 +682,95 @@ __device__ __forceinline__ void average_labels(const int32_t *nbr, int k, const 
     *l_out = sl / (float)k;
 }
 
-// One wave per query: gather the lists' entries (into LDS when they fit),
-// select the k smallest (key, index) pairs bit by bit from the most
-// significant key bit, order them, then gather and average the labels.
-template <bool PREDICT>
-__global__ __launch_bounds__(MERGE_WAVES * WAVE) void merge_kernel(const MergeArgs A)
+// One workgroup per query: gather the non-empty lists' entries into LDS (a
+// block-wide prefix sum places them), select the k smallest (key, index) pairs
+// bit by bit from the most significant key bit, order them, then gather and
+// average the labels. Entries that do not fit in LDS are read from the
+// workspace instead (slower, same result).
+template <int LPT, bool PREDICT>
+__global__ __launch_bounds__(MERGE_THREADS) void merge_kernel(const MergeArgs A)
 {
-    __shared__ uint32_t ek_all[MERGE_WAVES][MERGE_CAP];
-    __shared__ int32_t ei_all[MERGE_WAVES][MERGE_CAP];
-    __shared__ uint32_t sk_all[MERGE_WAVES][RB_MAX_K_DEV];
-    __shared__ int32_t si_all[MERGE_WAVES][RB_MAX_K_DEV];
-    __shared__ int32_t so_all[MERGE_WAVES][RB_MAX_K_DEV];
-    const int wave = threadIdx.x >> 6, lane = lane_id();
-    const int b = blockIdx.x * MERGE_WAVES + wave;
-    if (b >= A.B)
-        return;
+    __shared__ uint32_t ek[MERGE_CAP];
+    __shared__ int32_t ei[MERGE_CAP];
+    __shared__ int wsum[MERGE_THREADS / WAVE];
+    __shared__ int red[2][MERGE_THREADS / WAVE];
+    __shared__ uint32_t sk[RB_MAX_K_DEV];
+    __shared__ int32_t si[RB_MAX_K_DEV];
+    __shared__ int32_t so[RB_MAX_K_DEV];
+    __shared__ int ns_s;
+    const int tid = threadIdx.x, lane = lane_id(), wave = tid >> 6;
+    const int b = blockIdx.x;
     const int k = A.k, W = A.W;
-    uint32_t *ek = ek_all[wave];
-    int32_t *ei = ei_all[wave];
     const int32_t *cnt = A.ccnt + (size_t)b * W;
     const size_t base = (size_t)b * W * k;
 
-    // gather into LDS (entries past MERGE_CAP stay in global memory)
-    int total = 0;
-    for (int w0 = 0; w0 < W; w0 += WAVE) {
-        const int w = w0 + lane;
-        const int n = w < W ? cnt[w] : 0;
-        const int incl = wave_incl_scan(n);
-        const int off = total + incl - n;
-        for (int j = 0; j < n; ++j) {
-            if (off + j < MERGE_CAP) {
-                ek[off + j] = A.ckey[base + (size_t)w * k + j];
-                ei[off + j] = A.cidx[base + (size_t)w * k + j];
-            }
-        }
-        total += __shfl(incl, WAVE - 1);
+    // lists w = tid + MERGE_THREADS*u of this thread, their lengths and offsets
+    int n[LPT], mine = 0;
+#pragma unroll
+    for (int u = 0; u < LPT; ++u) {
+        const int w = tid + MERGE_THREADS * u;
+        n[u] = w < W ? cnt[w] : 0;
+        mine += n[u];
+    }
+    float incl = (float)mine;   // block prefix sum (counts < 2^24, exact in fp32)
+#pragma unroll
+    for (int m = 1; m < WAVE; m <<= 1) {
+        const float o = __shfl_up(incl, m);
+        if (lane >= m)
+            incl += o;
+    }
+    if (lane == WAVE - 1)
+        wsum[wave] = (int)incl;
+    if (tid == 0)
+        ns_s = 0;
+    __syncthreads();
+    int off = (int)incl - mine, total = 0;
+    for (int w = 0; w < MERGE_THREADS / WAVE; ++w) {
+        off += w < wave ? wsum[w] : 0;
+        total += wsum[w];
     }
     const bool in_lds = total <= MERGE_CAP;
-    // entry e of the gathered sequence: (key, idx)
+    if (in_lds) {
+#pragma unroll
+        for (int u = 0; u < LPT; ++u) {
+            const size_t o = base + (size_t)(tid + MERGE_THREADS * u) * k;
+            for (int j = 0; j < n[u]; ++j) {
+                ek[off + j] = A.ckey[o + j];
+                ei[off + j] = A.cidx[o + j];
+            }
+            off += n[u];
+        }
+    }
+    __syncthreads();
+
+    int phase = 0;
+    auto block_sum = [&](int c) -> int {
+        const float sw = wave_sum((float)c);
+        int *slot = red[phase & 1];
+        if (lane == 0)
+            slot[wave] = (int)sw;
+        __syncthreads();
+        ++phase;
+        int t = 0;
+#pragma unroll
+        for (int w = 0; w < MERGE_THREADS / WAVE; ++w)
+            t += slot[w];
+        return t;
+    };
     auto count_if = [&](auto pred) -> int {
         int c = 0;
         if (in_lds) {
-            for (int e = lane; e < total; e += WAVE)
+            for (int e = tid; e < total; e += MERGE_THREADS)
                 c += pred(ek[e], ei[e]);
         } else {
-            for (int w = 0; w < W; ++w) {
-                const int n = cnt[w];
-                if (lane < n)
-                    c += pred(A.ckey[base + (size_t)w * k + lane], A.cidx[base + (size_t)w * k + lane]);
+#pragma unroll
+            for (int u = 0; u < LPT; ++u) {
+                const size_t o = base + (size_t)(tid + MERGE_THREADS * u) * k;
+                for (int j = 0; j < n[u]; ++j)
+                    c += pred(A.ckey[o + j], A.cidx[o + j]);
             }
         }
-        return wave_sum_int(c);
+        return block_sum(c);
     };
     uint32_t prefix = 0;
     for (int bit = 31; bit >= 0; --bit) {
@@ -719,49 +787,43 @@ __global__ __launch_bounds__(MERGE_WAVES * WAVE) void merge_kernel(const MergeAr
         uint32_t up = 0;
         for (int bit = 30; bit >= 0; --bit) {
             const uint32_t trial = up | (1u << bit);
-            if (count_if([&](uint32_t kk, int32_t ii) { return kk == T && (uint32_t)ii < trial; }) < r)
+            if (count_if([&](uint32_t kk, int32_t ii) { return kk == T && (uint32_t)ii < trial; }) <
+                r)
                 up = trial;
         }
         U = (int32_t)up;
     }
-    // the k selected entries, compacted
-    uint32_t *sk = sk_all[wave];
-    int32_t *si = si_all[wave];
-    int32_t *so = so_all[wave];
-    if (lane < k) {
-        sk[lane] = KEY_NONE;
-        si[lane] = IDX_NONE;
-        so[lane] = IDX_NONE;
+    // the k selected entries, compacted (their order is fixed below)
+    if (tid < k) {
+        sk[tid] = KEY_NONE;
+        si[tid] = IDX_NONE;
+        so[tid] = IDX_NONE;
     }
-    int ns = 0;
-    auto take = [&](uint32_t kk, int32_t ii, bool valid) {
-        const bool s = valid && (kk < T || (kk == T && ii <= U));
-        const uint64_t m = ballot(s);
-        if (s) {
-            const int pos = ns + mbcnt(m);
+    __syncthreads();
+    auto take = [&](uint32_t kk, int32_t ii) {
+        if (kk < T || (kk == T && ii <= U)) {
+            const int pos = atomicAdd(&ns_s, 1);
             if (pos < k) {
                 sk[pos] = kk;
                 si[pos] = ii;
             }
         }
-        ns += popc(m);
     };
     if (in_lds) {
-        for (int e0 = 0; e0 < total; e0 += WAVE) {
-            const int e = e0 + lane;
-            take(e < total ? ek[e] : KEY_NONE, e < total ? ei[e] : IDX_NONE, e < total);
-        }
+        for (int e = tid; e < total; e += MERGE_THREADS)
+            take(ek[e], ei[e]);
     } else {
-        for (int w = 0; w < W; ++w) {
-            const int n = cnt[w];
-            take(lane < n ? A.ckey[base + (size_t)w * k + lane] : KEY_NONE,
-                 lane < n ? A.cidx[base + (size_t)w * k + lane] : IDX_NONE, lane < n);
+#pragma unroll
+        for (int u = 0; u < LPT; ++u) {
+            const size_t o = base + (size_t)(tid + MERGE_THREADS * u) * k;
+            for (int j = 0; j < n[u]; ++j)
+                take(A.ckey[o + j], A.cidx[o + j]);
         }
     }
-    // order by (key, index)
-    if (lane < k) {
-        const uint32_t mk = sk[lane];
-        const int32_t mi = si[lane];
+    __syncthreads();
+    if (tid < k) {
+        const uint32_t mk = sk[tid];
+        const int32_t mi = si[tid];
         int rank = 0;
         for (int j = 0; j < k; ++j)
             rank += (sk[j] < mk || (sk[j] == mk && si[j] < mi));
@@ -771,7 +833,8 @@ __global__ __launch_bounds__(MERGE_WAVES * WAVE) void merge_kernel(const MergeAr
         so[rank] = mi;
     }
     if constexpr (PREDICT) {
-        for (int m = lane; m < A.M; m += WAVE)
+        __syncthreads();
+        for (int m = tid; m < A.M; m += MERGE_THREADS)
             average_labels(so, k, A.qual, A.len, A.N, A.M, m, A.q_hat + (size_t)b * A.M + m,
                            A.l_hat + (size_t)b * A.M + m);
     }
@@ -810,28 +873,46 @@ size_t scan_lds_bytes(int ng, int k)
 
 thread_local hipEvent_t t_scan_begin = nullptr, t_scan_end = nullptr;
 
-template <int DT, int NG, int RT>
+template <int LPT>
+hipError_t launch_merge(const MergeArgs &m, int B, bool predict, hipStream_t s)
+{
+    if (predict)
+        hipLaunchKernelGGL((merge_kernel<LPT, true>), dim3(B), dim3(MERGE_THREADS), 0, s, m);
+    else
+        hipLaunchKernelGGL((merge_kernel<LPT, false>), dim3(B), dim3(MERGE_THREADS), 0, s, m);
+    return hipGetLastError();
+}
+
+template <int DT, int NG, bool RAGGED>
 hipError_t launch_scan(const ScanArgs &a, size_t lds, int grid, hipStream_t s)
 {
-    hipError_t e = hipFuncSetAttribute((const void *)scan_kernel<DT, NG, RT>,
+    auto kern = scan_kernel<DT, NG, SCAN_RT, RAGGED>;
+    hipError_t e = hipFuncSetAttribute((const void *)kern,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess)
         return e;
-    hipLaunchKernelGGL((scan_kernel<DT, NG, RT>), dim3(grid), dim3(SCAN_THREADS), lds, s, a);
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(SCAN_THREADS), lds, s, a);
     return hipGetLastError();
+}
+
+template <int DT, bool RAGGED>
+hipError_t launch_scan_r(const KnnPlan &p, const ScanArgs &a, int grid, hipStream_t s)
+{
+    switch (p.ng) {
+    case 16: return launch_scan<DT, 16, RAGGED>(a, p.lds_bytes, grid, s);
+    case 8: return launch_scan<DT, 8, RAGGED>(a, p.lds_bytes, grid, s);
+    case 4: return launch_scan<DT, 4, RAGGED>(a, p.lds_bytes, grid, s);
+    case 2: return launch_scan<DT, 2, RAGGED>(a, p.lds_bytes, grid, s);
+    case 1: return launch_scan<DT, 1, RAGGED>(a, p.lds_bytes, grid, s);
+    }
+    return hipErrorInvalidValue;
 }
 
 template <int DT>
 hipError_t launch_scan_dt(const KnnPlan &p, const ScanArgs &a, int grid, hipStream_t s)
 {
-    switch (p.ng) {
-    case 16: return launch_scan<DT, 16, SCAN_RT>(a, p.lds_bytes, grid, s);
-    case 8: return launch_scan<DT, 8, SCAN_RT>(a, p.lds_bytes, grid, s);
-    case 4: return launch_scan<DT, 4, SCAN_RT>(a, p.lds_bytes, grid, s);
-    case 2: return launch_scan<DT, 2, SCAN_RT>(a, p.lds_bytes, grid, s);
-    case 1: return launch_scan<DT, 1, SCAN_RT>(a, p.lds_bytes, grid, s);
-    }
-    return hipErrorInvalidValue;
+    const bool ragged = p.d % (4 * Elem<DT>::VEC) != 0;
+    return ragged ? launch_scan_r<DT, true>(p, a, grid, s) : launch_scan_r<DT, false>(p, a, grid, s);
 }
 
 template <int DT>
@@ -893,11 +974,21 @@ int plan_knn(int B, int N, int d, int dtype, int k, int num_cu, KnnPlan *p)
     const long max_chunks = ((long)N + 15) / 16;
     if (chunks > max_chunks)
         chunks = max_chunks;
+    const long rowb = (long)d * (dtype == 1 ? 2 : 4);
+    if ((long)B * rowb >= (1L << 31))
+        return -1;   // the query resource is addressed with 32-bit offsets
     long rpc = ((long)N + chunks - 1) / chunks;
     rpc = (rpc + 15) / 16 * 16;
+    while (rpc * rowb >= (1L << 31) - (1L << 20)) {   // so is each bank chunk
+        chunks *= 2;
+        rpc = ((long)N + chunks - 1) / chunks;
+        rpc = (rpc + 15) / 16 * 16;
+    }
     p->rows_per_chunk = rpc;
     p->n_chunks = (int)(((long)N + rpc - 1) / rpc);
     p->W = p->n_chunks * SCAN_WAVES;
+    if (p->W > MERGE_MAX_LISTS)
+        return -1;
     // seed sample: about N/32 rows, 2048..32768, a multiple of 64 and at most N
     long S = N / 32;
     if (S < 2048)
@@ -971,12 +1062,11 @@ hipError_t launch_knn(const KnnPlan &p, const void *queries, const void *bank,
         sa.G = p.G;
         sa.n_qg = (p.B + 15) / 16;
         sa.gmin = gmin;
-        const long waves = (long)sa.n_qg * (p.S / 64);
-        const int grid = (int)((waves + 3) / 4);
+        const dim3 grid(p.S / 64, (sa.n_qg + SEED_WAVES - 1) / SEED_WAVES);
         if (p.dtype == 1)
-            hipLaunchKernelGGL(seed_groups_kernel<1>, dim3(grid), dim3(256), 0, s, sa);
+            hipLaunchKernelGGL(seed_groups_kernel<1>, grid, dim3(SEED_WAVES * WAVE), 0, s, sa);
         else
-            hipLaunchKernelGGL(seed_groups_kernel<0>, dim3(grid), dim3(256), 0, s, sa);
+            hipLaunchKernelGGL(seed_groups_kernel<0>, grid, dim3(SEED_WAVES * WAVE), 0, s, sa);
         if ((e = hipGetLastError()) != hipSuccess)
             return e;
     }
@@ -1029,12 +1119,19 @@ hipError_t launch_knn(const KnnPlan &p, const void *queries, const void *bank,
     m.M = M;
     m.q_hat = q_hat;
     m.l_hat = l_hat;
-    const int mgrid = (p.B + MERGE_WAVES - 1) / MERGE_WAVES;
-    if (q_hat)
-        hipLaunchKernelGGL(merge_kernel<true>, dim3(mgrid), dim3(MERGE_WAVES * WAVE), 0, s, m);
-    else
-        hipLaunchKernelGGL(merge_kernel<false>, dim3(mgrid), dim3(MERGE_WAVES * WAVE), 0, s, m);
-    return hipGetLastError();
+    const int lpt = (p.W + MERGE_THREADS - 1) / MERGE_THREADS;
+    const bool pred = q_hat != nullptr;
+    if (lpt <= 1)
+        return launch_merge<1>(m, p.B, pred, s);
+    if (lpt <= 2)
+        return launch_merge<2>(m, p.B, pred, s);
+    if (lpt <= 4)
+        return launch_merge<4>(m, p.B, pred, s);
+    if (lpt <= 8)
+        return launch_merge<8>(m, p.B, pred, s);
+    if (lpt <= 16)
+        return launch_merge<16>(m, p.B, pred, s);
+    return hipErrorInvalidValue;
 }
 
 hipError_t launch_predict(const int32_t *nbr_idx, int B, int k, const float *bank_qual,

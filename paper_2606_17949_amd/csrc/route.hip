@@ -1,6 +1,12 @@
 // Request-instance scoring and the greedy online assignment (RouteBalance
 // Eq. 1 score, Eq. 2 cost, the dead-reckoned latency of Sec. 4.2, and the
 // greedy per-batch loop of Alg. 1), for gfx950.
+//
+// Both kernels evaluate the score with the same arithmetic (explicit fused
+// multiply-adds, reciprocal rates, and the two Eq. 1 ratios as IEEE divisions
+// so that the instance at a maximum gets exactly 1), so the dense score matrix
+// and the scores the greedy loop sees at the batch-start state agree bit for
+// bit.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -9,27 +15,34 @@ namespace rb {
 namespace {
 
 // Latency of a request with prompt l and predicted output lv on an instance
-// with queued prefill p, active decode a and rates P, D: the queued prefill
-// plus this prompt drains at P, then the active decode plus this output at D.
-__device__ __forceinline__ float latency(float p, float a, float P, float D, float l, float lv)
+// with queued prefill p, active decode a and reciprocal rates rP = 1/P,
+// rD = 1/D: the queued prefill plus this prompt drains at P, then the active
+// decode plus this output at D.
+__device__ __forceinline__ float latency(float p, float a, float rP, float rD, float l, float lv)
 {
-    return (p + l) / P + (a + lv) / D;
+    return fmaf(p + l, rP, (a + lv) * rD);
 }
 
 // Eq. 2 expected cost: input tokens at the input price plus predicted output
 // tokens at the output price.
 __device__ __forceinline__ float cost(float l, float lv, float cin, float cout)
 {
-    return l * cin + lv * cout;
+    return fmaf(l, cin, lv * cout);
 }
 
-// Eq. 1 with per-request maxima; a zero maximum makes its ratio 0.
-__device__ __forceinline__ float score_of(float qv, float C, float Cmax, float T, float Tmax,
-                                          float wq, float wl, float wc)
+// x / max, or 0 for a zero maximum.
+__device__ __forceinline__ float ratio(float x, float m) { return m > 0.f ? x / m : 0.f; }
+
+// The state-independent part of Eq. 1: w_qual*Q + w_cost*(1 - C/Cmax).
+__device__ __forceinline__ float base_score(float qv, float C, float cmax, float wq, float wc)
 {
-    const float rc = Cmax > 0.f ? C / Cmax : 0.f;
-    const float rt = Tmax > 0.f ? T / Tmax : 0.f;
-    return wq * qv + wc * (1.f - rc) + wl * (1.f - rt);
+    return fmaf(wq, qv, wc * (1.f - ratio(C, cmax)));
+}
+
+// Eq. 1: base + w_lat*(1 - T/Tmax).
+__device__ __forceinline__ float full_score(float base, float T, float tmax, float wl)
+{
+    return fmaf(wl, 1.f - ratio(T, tmax), base);
 }
 
 // One wave per request row of the dense score matrix.
@@ -46,109 +59,187 @@ __global__ __launch_bounds__(256) void score_kernel(const float *__restrict__ q_
     const float l = (float)plen[r];
     const float *qr = q_hat + (size_t)r * M;
     const float *lr = l_hat + (size_t)r * M;
+    const float nan = __builtin_nanf("");
     float cmax = -INFINITY, tmax = -INFINITY;
     for (int i = lane; i < I; i += WAVE) {
         const int m = in.model[i];
-        const float lv = (unsigned)m < (unsigned)M ? lr[m] : __builtin_nanf("");
+        const float lv = (unsigned)m < (unsigned)M ? lr[m] : nan;
         cmax = fmaxf(cmax, cost(l, lv, in.cin[i], in.cout[i]));
-        tmax = fmaxf(tmax, latency(in.p[i], in.a[i], in.P[i], in.D[i], l, lv));
+        tmax = fmaxf(tmax, latency(in.p[i], in.a[i], 1.f / in.P[i], 1.f / in.D[i], l, lv));
     }
     cmax = wave_max(cmax);
     tmax = wave_max(tmax);
     for (int i = lane; i < I; i += WAVE) {
         const int m = in.model[i];
         const bool mv = (unsigned)m < (unsigned)M;
-        const float lv = mv ? lr[m] : __builtin_nanf("");
-        const float qv = mv ? qr[m] : __builtin_nanf("");
+        const float lv = mv ? lr[m] : nan;
+        const float qv = mv ? qr[m] : nan;
         const float C = cost(l, lv, in.cin[i], in.cout[i]);
-        const float T = latency(in.p[i], in.a[i], in.P[i], in.D[i], l, lv);
-        S0[(size_t)r * I + i] = score_of(qv, C, cmax, T, tmax, wq, wl, wc);
+        const float T = latency(in.p[i], in.a[i], 1.f / in.P[i], 1.f / in.D[i], l, lv);
+        S0[(size_t)r * I + i] = full_score(base_score(qv, C, cmax, wq, wc), T, tmax, wl);
     }
 }
 
-// Greedy assignment on one wavefront. Instance i = lane + 64*u lives in
-// register slot u of its lane, with its state; each step is two wave maxima
-// (cost and latency), the scores, and an argmax with the lowest index among
-// equal scores, then the owner lane updates the chosen instance.
+// Greedy assignment. Wave 0 runs the sequential loop over requests; waves
+// 1..15 fill, one chunk of requests ahead, an LDS double buffer with what does
+// not depend on the state: per (request, instance) the base score and the
+// predicted output length on the instance's model. Instance i = lane + 64*u
+// lives in register slot u of wave 0's lane, with its state. Per request: the
+// latency maximum (one wave reduction), the scores, the largest score (one
+// wave reduction) and the lowest index holding it (a ballot), then the owner
+// lane updates the chosen instance.
+constexpr int ASSIGN_THREADS = 1024;
+constexpr int ASSIGN_WAVES = ASSIGN_THREADS / WAVE;
+constexpr int ASSIGN_LDS_FLOATS = 8192;   // per buffer: chunk rows x instances x 2
+
 template <int IPL>
-__global__ __launch_bounds__(64) void assign_kernel(const float *__restrict__ q_hat,
-                                                    const float *__restrict__ l_hat,
-                                                    const int32_t *__restrict__ plen, int B, int M,
-                                                    const InstArgs in, int I, float wq, float wl,
-                                                    float wc, int32_t *__restrict__ assign,
-                                                    float *__restrict__ chosen)
+__global__ __launch_bounds__(ASSIGN_THREADS) void assign_kernel(
+    const float *__restrict__ q_hat, const float *__restrict__ l_hat,
+    const int32_t *__restrict__ plen, int B, int M, const InstArgs in, int I, float wq, float wl,
+    float wc, int32_t *__restrict__ assign, float *__restrict__ chosen)
 {
-    const int lane = threadIdx.x;
-    int model[IPL];
-    float p[IPL], a[IPL], P[IPL], D[IPL], cin[IPL], cout[IPL];
+    constexpr int IP = IPL * WAVE;                        // padded instance count
+    constexpr int CH = ASSIGN_LDS_FLOATS / (2 * IP);      // requests per chunk
+    __shared__ float base_s[2][CH][IP];
+    __shared__ float lv_s[2][CH][IP];
+    __shared__ float l_s[2][CH];
+    const int lane = lane_id(), wave = threadIdx.x >> 6;
+    const int n_ch = (B + CH - 1) / CH;
+
+    // producers: request r of chunk c into buffer c & 1, one wave per request
+    auto produce = [&](int c) {
+        const int buf = c & 1;
+        for (int j = wave - 1; j < CH; j += ASSIGN_WAVES - 1) {
+            const int r = c * CH + j;
+            if (r >= B)
+                break;
+            const float l = (float)plen[r];
+            const float *qr = q_hat + (size_t)r * M;
+            const float *lr = l_hat + (size_t)r * M;
+            float qv[IPL], lv[IPL], C[IPL];
+            float cmax = -INFINITY;
+#pragma unroll
+            for (int u = 0; u < IPL; ++u) {
+                const int i = lane + WAVE * u;
+                const int m = i < I ? in.model[i] : -1;
+                const bool ok = (unsigned)m < (unsigned)M;
+                qv[u] = ok ? qr[m] : 0.f;
+                lv[u] = ok ? lr[m] : 0.f;
+                C[u] = cost(l, lv[u], ok ? in.cin[i] : 0.f, ok ? in.cout[i] : 0.f);
+                if (ok)
+                    cmax = fmaxf(cmax, C[u]);
+            }
+            cmax = wave_max(cmax);
+#pragma unroll
+            for (int u = 0; u < IPL; ++u) {
+                base_s[buf][j][lane + WAVE * u] = base_score(qv[u], C[u], cmax, wq, wc);
+                lv_s[buf][j][lane + WAVE * u] = lv[u];
+            }
+            if (lane == 0)
+                l_s[buf][j] = l;
+        }
+    };
+
+    if (wave > 0) {
+        produce(0);
+        __syncthreads();
+        for (int c = 0; c < n_ch; ++c) {
+            if (c + 1 < n_ch)
+                produce(c + 1);
+            __syncthreads();
+        }
+        return;
+    }
+
+    // consumer: instance state in registers
+    float p[IPL], a[IPL], rP[IPL], rD[IPL];
     bool valid[IPL];
 #pragma unroll
     for (int u = 0; u < IPL; ++u) {
         const int i = lane + WAVE * u;
         // an instance whose model id is outside [0, M) is never chosen
-        const int m = i < I ? in.model[i] : 0;
-        valid[u] = i < I && (unsigned)m < (unsigned)M;
-        model[u] = valid[u] ? m : 0;
+        const int m = i < I ? in.model[i] : -1;
+        valid[u] = (unsigned)m < (unsigned)M;
         p[u] = valid[u] ? in.p[i] : 0.f;
         a[u] = valid[u] ? in.a[i] : 0.f;
-        P[u] = valid[u] ? in.P[i] : 1.f;
-        D[u] = valid[u] ? in.D[i] : 1.f;
-        cin[u] = valid[u] ? in.cin[i] : 0.f;
-        cout[u] = valid[u] ? in.cout[i] : 0.f;
+        rP[u] = valid[u] ? 1.f / in.P[i] : 0.f;
+        rD[u] = valid[u] ? 1.f / in.D[i] : 0.f;
     }
-    for (int r = 0; r < B; ++r) {
-        const float l = (float)plen[r];
-        const float *qr = q_hat + (size_t)r * M;
-        const float *lr = l_hat + (size_t)r * M;
-        float qv[IPL], lv[IPL], C[IPL], T[IPL];
-        float cm = -INFINITY, tm = -INFINITY;
+    __syncthreads();   // chunk 0 is ready
+    for (int c = 0; c < n_ch; ++c) {
+        const int buf = c & 1;
+        const int rows = min(CH, B - c * CH);
+        float l = l_s[buf][0], bs[IPL], lv[IPL];
 #pragma unroll
         for (int u = 0; u < IPL; ++u) {
-            qv[u] = qr[model[u]];
-            lv[u] = lr[model[u]];
-            C[u] = cost(l, lv[u], cin[u], cout[u]);
-            T[u] = latency(p[u], a[u], P[u], D[u], l, lv[u]);
-            if (valid[u]) {
-                cm = fmaxf(cm, C[u]);
-                tm = fmaxf(tm, T[u]);
-            }
+            bs[u] = base_s[buf][0][lane + WAVE * u];
+            lv[u] = lv_s[buf][0][lane + WAVE * u];
         }
-        cm = wave_max(cm);
-        tm = wave_max(tm);
-        float best = -INFINITY;
-        int besti = 0x7fffffff;
-#pragma unroll
-        for (int u = 0; u < IPL; ++u) {
-            const float S = score_of(qv[u], C[u], cm, T[u], tm, wq, wl, wc);
-            if (valid[u] && S > best) {   // slots ascend in index, so ties keep the lower
-                best = S;
-                besti = lane + WAVE * u;
-            }
-        }
-        const float bs = wave_max(best);
-        // lowest index among lanes holding the maximum (indices < 2^24 are exact in fp32)
-        const float bi = -wave_max(best == bs ? -(float)besti : -INFINITY);
-        const int istar = (int)bi;
-        if (lane == 0) {
-            assign[r] = istar;
-            if (chosen)
-                chosen[r] = bs;
-        }
-        if ((istar & (WAVE - 1)) == lane) {
-            const int us = istar / WAVE;
+        for (int j = 0; j < rows; ++j) {
+            const int r = c * CH + j;
+            // next request's values, in flight while this one is decided
+            const int jn = j + 1 < rows ? j + 1 : j;
+            const float ln = l_s[buf][jn];
+            float bsn[IPL], lvn[IPL];
 #pragma unroll
             for (int u = 0; u < IPL; ++u) {
-                if (u == us) {
-                    p[u] += l;
-                    a[u] += lv[u];
+                bsn[u] = base_s[buf][jn][lane + WAVE * u];
+                lvn[u] = lv_s[buf][jn][lane + WAVE * u];
+            }
+            float T[IPL];
+            float tmax = -INFINITY;
+#pragma unroll
+            for (int u = 0; u < IPL; ++u) {
+                T[u] = latency(p[u], a[u], rP[u], rD[u], l, lv[u]);
+                if (valid[u])
+                    tmax = fmaxf(tmax, T[u]);
+            }
+            tmax = wave_max(tmax);
+            uint32_t best = 0;   // f2key of this lane's best score (0 = no candidate)
+            int bu = 0;
+#pragma unroll
+            for (int u = 0; u < IPL; ++u) {
+                const float S = full_score(bs[u], T[u], tmax, wl);
+                const uint32_t key = f2key(S);
+                if (valid[u] && S == S && key > best) {   // slots ascend in index: ties keep the lower
+                    best = key;
+                    bu = u;
                 }
             }
+            // largest score, then the lowest instance index holding it
+            const uint32_t kmax = wave_max_u32(best);
+            const uint32_t mine = (best == kmax && kmax != 0) ? (uint32_t)(lane + WAVE * bu) : ~0u;
+            const uint32_t imin = wave_min_u32(mine);
+            const bool found = kmax != 0;
+            const int istar = found ? (int)imin : 0;
+            const int wl_lane = istar & (WAVE - 1), wu = istar / WAVE;
+            if (lane == 0) {
+                assign[r] = istar;
+                if (chosen)
+                    chosen[r] = found ? key2f(kmax) : __builtin_nanf("");
+            }
+            if (found && lane == wl_lane) {
+#pragma unroll
+                for (int u = 0; u < IPL; ++u) {
+                    if (u == wu) {
+                        p[u] += l;
+                        a[u] += lv[u];
+                    }
+                }
+            }
+            l = ln;
+#pragma unroll
+            for (int u = 0; u < IPL; ++u) {
+                bs[u] = bsn[u];
+                lv[u] = lvn[u];
+            }
         }
+        __syncthreads();   // buffer c & 1 may now be refilled; chunk c + 1 is ready
     }
 #pragma unroll
     for (int u = 0; u < IPL; ++u) {
         const int i = lane + WAVE * u;
-        if (i < I) {
+        if (i < I && valid[u]) {
             in.p[i] = p[u];
             in.a[i] = a[u];
         }
@@ -181,8 +272,8 @@ hipError_t launch_assign(const float *q_hat, const float *l_hat, const int32_t *
 {
     const int ipl = (I + WAVE - 1) / WAVE;
 #define RB_ASSIGN(N)                                                                             \
-    hipLaunchKernelGGL(assign_kernel<N>, dim3(1), dim3(64), 0, s, q_hat, l_hat, plen, B, M, in, \
-                       I, wq, wl, wc, assign, chosen)
+    hipLaunchKernelGGL(assign_kernel<N>, dim3(1), dim3(ASSIGN_THREADS), 0, s, q_hat, l_hat,      \
+                       plen, B, M, in, I, wq, wl, wc, assign, chosen)
     if (ipl <= 1) RB_ASSIGN(1);
     else if (ipl <= 2) RB_ASSIGN(2);
     else if (ipl <= 4) RB_ASSIGN(4);
