@@ -9,10 +9,10 @@ namespace rb {
 
 constexpr int SCAN_THREADS = 256;   // 4 waves, one per SIMD
 constexpr int SCAN_WAVES = 4;
-constexpr int SCAN_RT = 4;         // 16-row MFMA tiles per wave per iteration (64 rows)
+constexpr int SCAN_RT = 3;         // 16-row MFMA tiles per wave per iteration (48 rows)
 constexpr int SCAN_PREFETCH = 3;    // k-steps whose loads are in flight ahead of the MFMAs
 constexpr int SCAN_UNROLL = 4;      // register ring of bank fragments; k-steps are padded to it
-constexpr int STAGE_CAP = 256;      // per-wave staging: one (query group, row tile) of candidates
+constexpr int STAGE_CAP = 256;      // per-wave LDS staging of one iteration's candidates
 constexpr size_t LDS_LIMIT = 160 * 1024;
 constexpr int MERGE_THREADS = 256;  // one query per workgroup
 constexpr int MERGE_CAP = 4096;     // candidates per query the merge holds in LDS
@@ -24,21 +24,25 @@ constexpr int SEED_MAX_GROUPS = 2048;
 //  * seed: S bank rows spread evenly over the bank; per query, the k-th
 //    smallest of the S/16 minima over groups of 16 of them bounds the k-th
 //    nearest distance from above (k distinct rows lie at or below it).
-//  * scan: query tiles of 16*ng queries; the bank in n_chunks contiguous row
-//    ranges (multiples of 16 rows); one workgroup per (chunk, tile); each of
-//    its 4 waves owns 16*rt rows per iteration and keeps, per query, a list of
-//    at most k candidates that pass the bound.
-//  * merge: per query, the k smallest of its 4*n_chunks lists.
+//  * scan: query tiles of 16*ng queries, whose first gr groups stay in LDS
+//    for the whole call while the others stream through it; the
+//    bank in n_chunks contiguous row ranges (multiples of 16 rows); one
+//    workgroup per (chunk, tile); each of its 4 waves owns 16*rt rows per
+//    iteration; the workgroup keeps, per query, one list of the k best
+//    candidates that pass the bound.
+//  * merge: per query, the k smallest of its W = n_chunks lists.
 struct KnnPlan {
     int dtype;          // 0 fp32, 1 bf16
     int B, N, d, k;
     int nks, nksp;      // 64-byte k-steps per row, padded to SCAN_UNROLL
-    int ng, rt;         // query groups of 16 per tile, 16-row tiles per wave
+    int ng, gr, rt;     // query groups of 16 per tile (gr of them resident), 16-row tiles per wave
     int n_qt, n_chunks, W;
     long rows_per_chunk;
     int S, G;           // seed rows and groups (0 = no seed)
+    int grid;           // scan workgroups
+    int ovf_cap;        // candidates per scan wave that the workspace takes past LDS
     size_t lds_bytes;
-    size_t off_tau, off_qn, off_gmin, off_ccnt, off_ckey, off_cidx, bytes;
+    size_t off_tau, off_qn, off_gmin, off_ccnt, off_ckey, off_cidx, off_ovf, bytes;
 };
 
 int plan_knn(int B, int N, int d, int dtype, int k, int num_cu, KnnPlan *p);

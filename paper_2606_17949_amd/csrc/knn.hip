@@ -6,12 +6,13 @@
 //                       over the bank; minima over groups of 16 of those rows
 //   seed_bound_kernel   per query: |q|^2, and the k-th smallest group minimum
 //                       as the starting bound of the k-th nearest distance
-//   scan_kernel         the bank once through MFMA: one workgroup per (bank
-//                       chunk, tile of up to 256 queries); bank rows go from
-//                       HBM straight into MFMA operand registers, the query
-//                       tile streams through an LDS double buffer along K; a
-//                       register-level test against the per-query bound lets
-//                       only candidates reach the per-wave top-k lists
+//   scan_kernel         the bank once through MFMA (scan.hpp): one workgroup
+//                       per (bank chunk, tile of up to 256 queries); bank rows
+//                       go from HBM straight into MFMA operand registers, the
+//                       query tile sits in LDS (part resident, part streamed
+//                       along K); a register-level test against the per-query
+//                       bound lets only candidates reach the workgroup's
+//                       shared top-k lists
 //   merge_kernel        per query: the k nearest of all lists, sorted, then
 //                       optionally the label gather and average (Sec. 4.2: one
 //                       lookup predicts quality and length for every model)
@@ -19,151 +20,11 @@
 // index. Distances are |q|^2 + |x|^2 - 2<q,x> with fp32 products and
 // accumulation; the scan accumulates -|x|^2/2 + <q,x> and reports
 // |q|^2 - 2*acc.
-#include <float.h>
-
-#include "common.hpp"
-#include "kernels.hpp"
+#include "knn_common.hpp"
 
 namespace rb {
 
 namespace {
-
-template <int DT> struct Elem;
-template <> struct Elem<0> { static constexpr int VEC = 4, ESZ = 4; };   // fp32
-template <> struct Elem<1> { static constexpr int VEC = 8, ESZ = 2; };   // bf16
-
-constexpr int KSTEP_BYTES = 64;   // bytes of one row in one k-step (4 lanes x 16 bytes)
-
-// Sum of squares of the 16-byte group held in v, added to s in element order.
-template <int DT>
-__device__ __forceinline__ float sumsq16(const i32x4 &v, float s)
-{
-    if constexpr (DT == 1) {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const uint32_t w = (uint32_t)v[e];
-            const float x0 = bf16lo(w), x1 = bf16hi(w);
-            s = fmaf(x0, x0, s);
-            s = fmaf(x1, x1, s);
-        }
-    } else {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const float x = __int_as_float(v[e]);
-            s = fmaf(x, x, s);
-        }
-    }
-    return s;
-}
-
-// One 16x16 MFMA tile step over 16 bytes of K per lane, D = A*B + C:
-//   bf16: one v_mfma_f32_16x16x32_bf16 (8 elements per lane)
-//   fp32: four v_mfma_f32_16x16x4_f32 (element e of every lane in step e)
-// A and B hold the same K positions in the same lanes, so the dot products
-// come out right whatever order the hardware assigns K within a step.
-template <int DT>
-__device__ __forceinline__ f32x4 mfma_step(const i32x4 &a, const i32x4 &b, const f32x4 &c)
-{
-    if constexpr (DT == 1) {
-        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
-                                                       __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
-    } else {
-        f32x4 d = c;
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-            d = __builtin_amdgcn_mfma_f32_16x16x4f32(__int_as_float(a[e]), __int_as_float(b[e]), d,
-                                                     0, 0, 0);
-        return d;
-    }
-}
-
-__device__ __forceinline__ i32x4 load16(const uint8_t *p) { return *(const i32x4 *)p; }
-
-// Raw buffer resource over [base, base + bytes): loads at or past the end
-// return zero, which masks rows past a chunk and queries past the batch.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, uint32_t bytes)
-{
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes,
-                                             0x00020000);
-}
-
-__device__ __forceinline__ i32x4 buffer_load16(__amdgpu_buffer_rsrc_t r, uint32_t voffset)
-{
-    return __builtin_bit_cast(i32x4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)voffset, 0, 0));
-}
-
-constexpr uint32_t OFF_NONE = 0x80000000u;   // a buffer offset past any resource
-
-template <int I> struct Int {
-    static constexpr int value = I;
-};
-
-// f(Int<I>) for I = B..E-1, unrolled at compile time.
-template <int B, int E, typename F>
-__device__ __forceinline__ void static_for(F &&f)
-{
-    if constexpr (B < E) {
-        f(Int<B>{});
-        static_for<B + 1, E>(f);
-    }
-}
-
-// Workgroup barrier that orders LDS only (waits for this wave's LDS traffic),
-// leaving global loads in flight across it.
-__device__ __forceinline__ void lds_barrier()
-{
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-}
-
-__device__ __forceinline__ uint32_t lds_load_relaxed(const uint32_t *p)
-{
-    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-}
-
-__device__ __forceinline__ void lds_store_relaxed(uint32_t *p, uint32_t v)
-{
-    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-}
-
-__device__ __forceinline__ uint64_t pack(uint32_t key, int32_t idx)
-{
-    return ((uint64_t)key << 32) | (uint32_t)idx;
-}
-
-__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v)
-{
-#pragma unroll
-    for (int m = 1; m < WAVE; m <<= 1) {
-        const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, m);
-        const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), m);
-        const uint64_t o = ((uint64_t)hi << 32) | lo;
-        v = o > v ? o : v;
-    }
-    return v;
-}
-
-// Inclusive prefix sum over the wave.
-__device__ __forceinline__ int wave_incl_scan(int v)
-{
-    const int lane = lane_id();
-#pragma unroll
-    for (int m = 1; m < WAVE; m <<= 1) {
-        const int o = __shfl_up(v, m);
-        if (lane >= m)
-            v += o;
-    }
-    return v;
-}
-
-__device__ __forceinline__ int wave_sum_int(int v)
-{
-#pragma unroll
-    for (int m = 1; m < WAVE; m <<= 1)
-        v += __shfl_xor(v, m);
-    return v;
-}
 
 // ------------------------------------------------------------------ norms
 
@@ -295,354 +156,6 @@ __global__ __launch_bounds__(256) void seed_bound_kernel(const uint8_t *__restri
     if (lane == 0) {
         qn[b] = s;
         tau[b] = T;
-    }
-}
-
-// ------------------------------------------------------------------ scan
-
-struct ScanArgs {
-    const uint8_t *queries, *bank;
-    const float *bank_norms, *qn;
-    int B, N, d, k, nks, nksp, n_chunks, n_qt, W;
-    long rows_per_chunk;
-    uint32_t *tau;    // [B] shared bound (distance keys), lowered with atomicMin
-    int32_t *ccnt;    // [B][W] list lengths
-    uint32_t *ckey;   // [B][W][k]
-    int32_t *cidx;    // [B][W][k]
-};
-
-template <int DT, int NG, int RT, bool RAGGED>
-__global__ __launch_bounds__(SCAN_THREADS, 1) void scan_kernel(const ScanArgs A)
-{
-    constexpr int BM = NG * 16;
-    constexpr int VEC = Elem<DT>::VEC, ESZ = Elem<DT>::ESZ;
-    constexpr int KS = 4 * VEC;                    // elements of one k-step
-    constexpr int RW = RT * 16;                    // rows per wave per iteration
-    constexpr int RWG = SCAN_WAVES * RW;           // rows per workgroup iteration
-    constexpr int QITEMS = NG * WAVE;              // 16-byte query items of one k-step
-    constexpr int QPT = (QITEMS + SCAN_THREADS - 1) / SCAN_THREADS;
-    constexpr int R = SCAN_UNROLL, P = SCAN_PREFETCH;
-    static_assert(P < R, "prefetch distance must leave a free ring slot");
-    static_assert(RW == WAVE, "one bank-norm load per lane per iteration");
-
-    extern __shared__ __align__(16) uint8_t smem[];
-    const int k = A.k;
-    i32x4 *qbuf = (i32x4 *)smem;                                    // [2][NG][64]
-    float *qn_s = (float *)(qbuf + 2 * QITEMS);                     // [BM]
-    uint32_t *gb_s = (uint32_t *)(qn_s + BM);                       // [BM] shared-bound snapshot
-    float *nx_all = (float *)(gb_s + BM);                           // [4][2][RW] -|x|^2/2
-    uint32_t *lk_all = (uint32_t *)(nx_all + SCAN_WAVES * 2 * RW);  // [4][BM][k]
-    int32_t *li_all = (int32_t *)(lk_all + SCAN_WAVES * BM * k);    // [4][BM][k]
-    int *lc_all = (int *)(li_all + SCAN_WAVES * BM * k);            // [4][BM]
-    uint32_t *lmk_all = (uint32_t *)(lc_all + SCAN_WAVES * BM);     // [4][BM] max key of a full list
-    int32_t *lmi_all = (int32_t *)(lmk_all + SCAN_WAVES * BM);      // [4][BM] its index
-    int *sq_all = (int *)(lmi_all + SCAN_WAVES * BM);               // [4][STAGE_CAP]
-    uint32_t *sk_all = (uint32_t *)(sq_all + SCAN_WAVES * STAGE_CAP);
-    int32_t *si_all = (int32_t *)(sk_all + SCAN_WAVES * STAGE_CAP);
-
-    // Workgroup -> (chunk c, query tile t). Workgroups are dispatched to the
-    // eight XCDs round robin, so this map puts every query tile of one chunk
-    // on the same XCD, where they share that chunk's lines in L2.
-    const int per8 = 8 * A.n_qt;
-    const int rem = blockIdx.x % per8;
-    const int t = rem / 8;
-    const int c = (blockIdx.x / per8) * 8 + rem % 8;
-    if (c >= A.n_chunks)
-        return;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int col = lane & 15, jg = lane >> 4;
-    const int q0 = t * BM;
-    const long rbeg = (long)c * A.rows_per_chunk;
-    const long rend = min((long)A.N, rbeg + A.rows_per_chunk);
-    const int n_it = rend > rbeg ? (int)((rend - rbeg + RWG - 1) / RWG) : 0;
-    const int nks = A.nks, nksp = A.nksp;
-    const size_t rowb = (size_t)A.d * ESZ;
-
-    float *nx = nx_all + wave * 2 * RW;
-    uint32_t *lk = lk_all + wave * BM * k;
-    int32_t *li = li_all + wave * BM * k;
-    int *lc = lc_all + wave * BM;
-    uint32_t *lmk = lmk_all + wave * BM;
-    int32_t *lmi = lmi_all + wave * BM;
-    int *sq = sq_all + wave * STAGE_CAP;
-    uint32_t *sk = sk_all + wave * STAGE_CAP;
-    int32_t *si = si_all + wave * STAGE_CAP;
-
-    for (int i = tid; i < BM; i += SCAN_THREADS) {
-        const int q = q0 + i;
-        qn_s[i] = q < A.B ? A.qn[q] : 0.f;
-        gb_s[i] = q < A.B ? A.tau[q] : 0u;
-    }
-    for (int i = tid; i < SCAN_WAVES * BM; i += SCAN_THREADS)
-        lc_all[i] = 0;
-
-    // ---- loads of one k-step through buffer resources whose base moves by one
-    // k-step (64 bytes of a row) per step; each lane keeps a fixed offset. Rows
-    // past the chunk and queries past the batch fall outside the resource and
-    // load zero; so does every lane of a padding k-step (empty resource). The
-    // query items run two k-steps ahead of the MFMAs, the bank rows three.
-    const uint8_t *bank_c = A.bank + (size_t)rbeg * rowb;
-    const uint32_t bank_c_bytes = (uint32_t)((rend - rbeg) * (long)rowb);
-    const uint32_t q_bytes = (uint32_t)((size_t)A.B * rowb);
-    uint32_t qvo[QPT];   // per item: q*rowb + (l/16)*16, or OFF_NONE
-    int qkk[QPT];        // element offset of the item within a k-step
-#pragma unroll
-    for (int i = 0; i < QPT; ++i) {
-        const int item = tid + SCAN_THREADS * i;
-        const int f = item >> 6, l = item & 63;
-        const int q = q0 + f * 16 + (l & 15);
-        qkk[i] = (l >> 4) * VEC;
-        qvo[i] = item < QITEMS ? (uint32_t)((size_t)q * rowb + (l >> 4) * 16) : OFF_NONE;
-    }
-    int pq_s = 0;             // k-step of the next query load (every iteration is the same)
-    int pb_it = 0, pb_s = 0;  // k-step of the next bank load
-    uint32_t bvo = (uint32_t)((size_t)(wave * RW + col) * rowb + jg * 16);   // tile 0 of pb_it
-    auto issue_q = [&](i32x4(&qs)[QPT]) {
-        const bool real = pq_s < nks;
-        const __amdgpu_buffer_rsrc_t r =
-            make_rsrc(A.queries + pq_s * KSTEP_BYTES, real ? q_bytes - pq_s * KSTEP_BYTES : 0u);
-#pragma unroll
-        for (int i = 0; i < QPT; ++i) {
-            uint32_t vo = qvo[i];
-            if constexpr (RAGGED)
-                vo = pq_s * KS + qkk[i] < A.d ? vo : OFF_NONE;
-            qs[i] = buffer_load16(r, vo);
-        }
-        if (++pq_s == nksp)
-            pq_s = 0;
-    };
-    auto issue_b = [&](i32x4(&a)[RT]) {
-        const bool real = pb_it < n_it && pb_s < nks;
-        const __amdgpu_buffer_rsrc_t r = make_rsrc(
-            bank_c + pb_s * KSTEP_BYTES, real ? bank_c_bytes - pb_s * KSTEP_BYTES : 0u);
-        const bool lane_ok = !RAGGED || pb_s * KS + jg * VEC < A.d;
-#pragma unroll
-        for (int tt = 0; tt < RT; ++tt)
-            a[tt] = buffer_load16(r, lane_ok ? bvo + (uint32_t)(tt * 16 * rowb) : OFF_NONE);
-        if (++pb_s == nksp) {
-            pb_s = 0;
-            ++pb_it;
-            bvo += (uint32_t)(RWG * rowb);
-        }
-    };
-    auto stage_queries = [&](int slot, const i32x4(&qs)[QPT]) {
-#pragma unroll
-        for (int i = 0; i < QPT; ++i) {
-            const int item = tid + SCAN_THREADS * i;
-            if (item < QITEMS)
-                qbuf[slot * QITEMS + item] = qs[i];
-        }
-    };
-    // -|x|^2/2 of bank row `lane` of this wave in iteration it (-inf past the chunk)
-    auto load_norm = [&](int it) -> float {
-        const long row = rbeg + (long)it * RWG + wave * RW + lane;
-        const bool v = it < n_it && row < rend;
-        const float xn = A.bank_norms[v ? row : 0];
-        return v ? -0.5f * xn : -INFINITY;
-    };
-    // Filter threshold of tile query i: a value is a candidate if acc >= nu (a
-    // superset of distance <= the query's bound; the exact test follows on
-    // insertion).
-    auto nu_of = [&](int i) -> float {
-        if (q0 + i >= A.B)
-            return INFINITY;
-        uint32_t tk = lds_load_relaxed(gb_s + i);
-        if (lc[i] == k)
-            tk = min(tk, lmk[i]);
-        if (tk == KEY_NONE)
-            return -FLT_MAX;
-        const float qq = qn_s[i], th = key2f(tk);
-        const float v = 0.5f * (qq - th);
-        return v - ldexpf(fabsf(qq) + fabsf(th) + fabsf(v), -21);
-    };
-    auto recompute_max = [&](int i) {
-        const uint64_t v = lane < k ? pack(lk[i * k + lane], li[i * k + lane]) : 0;
-        const uint64_t m = wave_max_u64(v);
-        if (lane == 0) {
-            lmk[i] = (uint32_t)(m >> 32);
-            lmi[i] = (int32_t)(uint32_t)m;
-            atomicMin(A.tau + q0 + i, (uint32_t)(m >> 32));
-        }
-    };
-    // Insert (key, idx) into this wave's list of tile query i (wave-uniform call).
-    auto insert = [&](int i, uint32_t key, int32_t idx) {
-        if (key > lds_load_relaxed(gb_s + i))
-            return;
-        const int n = lc[i];
-        if (n < k) {
-            if (lane == 0) {
-                lk[i * k + n] = key;
-                li[i * k + n] = idx;
-                lc[i] = n + 1;
-            }
-            if (n + 1 == k)
-                recompute_max(i);
-            return;
-        }
-        const uint32_t mk = lmk[i];
-        const int32_t mi = lmi[i];
-        if (!(key < mk || (key == mk && idx < mi)))
-            return;
-        if (lane < k && lk[i * k + lane] == mk && li[i * k + lane] == mi) {
-            lk[i * k + lane] = key;
-            li[i * k + lane] = idx;
-        }
-        recompute_max(i);
-    };
-    auto flush = [&](int n) {
-        for (int s = 0; s < n; ++s) {
-            const int i = __builtin_amdgcn_readfirstlane(sq[s]);
-            const uint32_t key = (uint32_t)__builtin_amdgcn_readfirstlane((int)sk[s]);
-            const int32_t idx = __builtin_amdgcn_readfirstlane(si[s]);
-            insert(i, key, idx);
-        }
-    };
-
-    f32x4 acc[RT][NG];
-    i32x4 ring[R][RT];
-    i32x4 qst[2][QPT];
-    int x = 0;   // global k-step index of the MFMAs
-    const int total = n_it * nksp;
-
-    // One block of R k-steps.
-    auto block = [&]() {
-#pragma unroll
-        for (int u = 0; u < R; ++u) {
-            if (x > 0)
-                lds_barrier();
-            if (x + 1 < total)
-                stage_queries((u + 1) & 1, qst[(u + 1) & 1]);
-            issue_q(qst[u & 1]);
-            issue_b(ring[(u + P) % R]);
-            const i32x4 *qb = qbuf + (u & 1) * QITEMS;
-            i32x4 b = qb[lane];
-#pragma unroll
-            for (int g = 0; g < NG; ++g) {
-                const i32x4 bn = qb[((g + 1) % NG) * WAVE + lane];   // next fragment, in flight
-#pragma unroll
-                for (int tt = 0; tt < RT; ++tt)
-                    acc[tt][g] = mfma_step<DT>(ring[u][tt], b, acc[tt][g]);
-                b = bn;
-            }
-            ++x;
-        }
-    };
-
-    // ---- pipeline prologue
-#pragma unroll
-    for (int u = 0; u < P; ++u)
-        issue_b(ring[u]);
-    issue_q(qst[0]);
-    issue_q(qst[1]);
-    stage_queries(0, qst[0]);
-    nx[lane] = load_norm(0);
-    float nx_next = load_norm(1);
-    lds_barrier();
-
-    for (int it = 0; it < n_it; ++it) {
-        // the accumulators start from -|x|^2/2 of their rows
-#pragma unroll
-        for (int tt = 0; tt < RT; ++tt) {
-            const f32x4 nxh = *(const f32x4 *)(nx + (it & 1) * RW + tt * 16 + jg * 4);
-#pragma unroll
-            for (int g = 0; g < NG; ++g)
-                acc[tt][g] = nxh;
-        }
-        for (int s0 = 0; s0 < nksp; s0 += R)
-            block();
-
-        // ---- end of iteration `it`: acc = -|x|^2/2 + <q, x>; dist = |q|^2 - 2*acc
-        nx[((it + 1) & 1) * RW + lane] = nx_next;
-        nx_next = load_norm(it + 2);
-        uint64_t any = 0;
-        static_for<0, NG>([&](auto G) {
-            constexpr int g = decltype(G)::value;
-            float m = -INFINITY;
-            static_for<0, RT>([&](auto TT) {
-                constexpr int tt = decltype(TT)::value;
-                m = fmaxf(m, fmaxf(fmaxf(acc[tt][g][0], acc[tt][g][1]),
-                                   fmaxf(acc[tt][g][2], acc[tt][g][3])));
-            });
-            any |= ballot(m >= nu_of(g * 16 + col));
-        });
-        if (any) {
-            const long wr0 = rbeg + (long)it * RWG + wave * RW;
-            // Stage the candidates of one (query group, row tile) in LDS; the
-            // switch keeps every accumulator access at a compile-time index.
-            auto stage = [&](auto G, auto TT) -> int {
-                constexpr int g = decltype(G)::value, tt = decltype(TT)::value;
-                const int i = g * 16 + col;
-                const float nu = nu_of(i);
-                const f32x4 a4 = acc[tt][g];
-                if (!ballot(fmaxf(fmaxf(a4[0], a4[1]), fmaxf(a4[2], a4[3])) >= nu))
-                    return 0;
-                const float qq = qn_s[i];
-                int nst = 0;
-                static_for<0, 4>([&](auto E) {
-                    constexpr int e = decltype(E)::value;
-                    const bool cnd = a4[e] >= nu;
-                    const uint64_t m = ballot(cnd);
-                    if (cnd) {
-                        const int pos = nst + mbcnt(m);
-                        sq[pos] = i;
-                        sk[pos] = f2key(fmaf(-2.f, a4[e], qq));
-                        si[pos] = (int32_t)(wr0 + tt * 16 + jg * 4 + e);
-                    }
-                    nst += popc(m);
-                });
-                return nst;
-            };
-            for (int gt = 0; gt < NG * RT; ++gt) {
-                int nst = 0;
-                switch (gt) {
-#define RB_STAGE_CASE(GT)                                                                          \
-    case GT:                                                                                       \
-        if constexpr (GT < NG * RT)                                                                \
-            nst = stage(Int<GT / RT>{}, Int<GT % RT>{});                                           \
-        break;
-                    RB_STAGE_CASE(0) RB_STAGE_CASE(1) RB_STAGE_CASE(2) RB_STAGE_CASE(3)
-                    RB_STAGE_CASE(4) RB_STAGE_CASE(5) RB_STAGE_CASE(6) RB_STAGE_CASE(7)
-                    RB_STAGE_CASE(8) RB_STAGE_CASE(9) RB_STAGE_CASE(10) RB_STAGE_CASE(11)
-                    RB_STAGE_CASE(12) RB_STAGE_CASE(13) RB_STAGE_CASE(14) RB_STAGE_CASE(15)
-                    RB_STAGE_CASE(16) RB_STAGE_CASE(17) RB_STAGE_CASE(18) RB_STAGE_CASE(19)
-                    RB_STAGE_CASE(20) RB_STAGE_CASE(21) RB_STAGE_CASE(22) RB_STAGE_CASE(23)
-                    RB_STAGE_CASE(24) RB_STAGE_CASE(25) RB_STAGE_CASE(26) RB_STAGE_CASE(27)
-                    RB_STAGE_CASE(28) RB_STAGE_CASE(29) RB_STAGE_CASE(30) RB_STAGE_CASE(31)
-                    RB_STAGE_CASE(32) RB_STAGE_CASE(33) RB_STAGE_CASE(34) RB_STAGE_CASE(35)
-                    RB_STAGE_CASE(36) RB_STAGE_CASE(37) RB_STAGE_CASE(38) RB_STAGE_CASE(39)
-                    RB_STAGE_CASE(40) RB_STAGE_CASE(41) RB_STAGE_CASE(42) RB_STAGE_CASE(43)
-                    RB_STAGE_CASE(44) RB_STAGE_CASE(45) RB_STAGE_CASE(46) RB_STAGE_CASE(47)
-                    RB_STAGE_CASE(48) RB_STAGE_CASE(49) RB_STAGE_CASE(50) RB_STAGE_CASE(51)
-                    RB_STAGE_CASE(52) RB_STAGE_CASE(53) RB_STAGE_CASE(54) RB_STAGE_CASE(55)
-                    RB_STAGE_CASE(56) RB_STAGE_CASE(57) RB_STAGE_CASE(58) RB_STAGE_CASE(59)
-                    RB_STAGE_CASE(60) RB_STAGE_CASE(61) RB_STAGE_CASE(62) RB_STAGE_CASE(63)
-#undef RB_STAGE_CASE
-                }
-                if (nst)
-                    flush(nst);
-            }
-        }
-        // pick up bounds other workgroups have lowered
-        for (int i = tid; i < BM; i += SCAN_THREADS)
-            if (q0 + i < A.B)
-                lds_store_relaxed(gb_s + i, __hip_atomic_load(A.tau + q0 + i, __ATOMIC_RELAXED,
-                                                              __HIP_MEMORY_SCOPE_AGENT));
-    }
-
-    // ---- this wave's lists -> workspace [B][W][k]
-    const int wl = c * SCAN_WAVES + wave;
-    for (int i = 0; i < BM; ++i) {
-        const int q = q0 + i;
-        if (q >= A.B)
-            break;
-        const int n = lc[i];
-        const size_t o = (size_t)q * A.W + wl;
-        if (lane == 0)
-            A.ccnt[o] = n;
-        if (lane < n) {
-            A.ckey[o * k + lane] = lk[i * k + lane];
-            A.cidx[o * k + lane] = li[i * k + lane];
-        }
     }
 }
 
@@ -860,17 +373,6 @@ __global__ __launch_bounds__(64) void predict_kernel(const int32_t *__restrict__
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-size_t scan_lds_bytes(int ng, int k)
-{
-    const size_t bm = (size_t)ng * 16;
-    return 2 * (size_t)ng * WAVE * 16 +   // query double buffer: 2 x ng fragments of 1 KB
-           bm * 8 +                       // |q|^2, bound snapshot
-           (size_t)SCAN_WAVES * 2 * SCAN_RT * 16 * 4 +   // bank norms of two iterations
-           (size_t)SCAN_WAVES * bm * k * 8 +   // lists
-           (size_t)SCAN_WAVES * bm * 12 +      // counts, max key, max index
-           (size_t)SCAN_WAVES * STAGE_CAP * 12;
-}
-
 thread_local hipEvent_t t_scan_begin = nullptr, t_scan_end = nullptr;
 
 template <int LPT>
@@ -881,38 +383,6 @@ hipError_t launch_merge(const MergeArgs &m, int B, bool predict, hipStream_t s)
     else
         hipLaunchKernelGGL((merge_kernel<LPT, false>), dim3(B), dim3(MERGE_THREADS), 0, s, m);
     return hipGetLastError();
-}
-
-template <int DT, int NG, bool RAGGED>
-hipError_t launch_scan(const ScanArgs &a, size_t lds, int grid, hipStream_t s)
-{
-    auto kern = scan_kernel<DT, NG, SCAN_RT, RAGGED>;
-    hipError_t e = hipFuncSetAttribute((const void *)kern,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess)
-        return e;
-    hipLaunchKernelGGL(kern, dim3(grid), dim3(SCAN_THREADS), lds, s, a);
-    return hipGetLastError();
-}
-
-template <int DT, bool RAGGED>
-hipError_t launch_scan_r(const KnnPlan &p, const ScanArgs &a, int grid, hipStream_t s)
-{
-    switch (p.ng) {
-    case 16: return launch_scan<DT, 16, RAGGED>(a, p.lds_bytes, grid, s);
-    case 8: return launch_scan<DT, 8, RAGGED>(a, p.lds_bytes, grid, s);
-    case 4: return launch_scan<DT, 4, RAGGED>(a, p.lds_bytes, grid, s);
-    case 2: return launch_scan<DT, 2, RAGGED>(a, p.lds_bytes, grid, s);
-    case 1: return launch_scan<DT, 1, RAGGED>(a, p.lds_bytes, grid, s);
-    }
-    return hipErrorInvalidValue;
-}
-
-template <int DT>
-hipError_t launch_scan_dt(const KnnPlan &p, const ScanArgs &a, int grid, hipStream_t s)
-{
-    const bool ragged = p.d % (4 * Elem<DT>::VEC) != 0;
-    return ragged ? launch_scan_r<DT, true>(p, a, grid, s) : launch_scan_r<DT, false>(p, a, grid, s);
 }
 
 template <int DT>
@@ -949,21 +419,31 @@ int plan_knn(int B, int N, int d, int dtype, int k, int num_cu, KnnPlan *p)
     p->k = k;
     p->nks = (d + 4 * vec - 1) / (4 * vec);
     p->nksp = (p->nks + SCAN_UNROLL - 1) / SCAN_UNROLL * SCAN_UNROLL;
-    // largest query tile that B can fill and that fits in LDS
+    // largest query tile that B can fill and whose lists fit in LDS; then as
+    // many of its query groups resident in LDS as the rest of the space holds
     int want = 1;
     while (want < 16 && want * 16 < B)
         want *= 2;
     p->ng = 0;
     for (int ng = want; ng >= 1; ng /= 2) {
-        const size_t lds = scan_lds_bytes(ng, k);
-        if (lds <= LDS_LIMIT) {
+        if (scan_layout(ng, 0, p->nksp, k, SCAN_RT).bytes <= LDS_LIMIT) {
             p->ng = ng;
-            p->lds_bytes = lds;
             break;
         }
     }
     if (p->ng == 0)
         return -1;
+    // resident query groups: all, half, a quarter or none of the tile (the
+    // counts the scan is compiled for), the most that fit
+    const int gr_opts[4] = {p->ng, p->ng / 2, p->ng / 4, 0};
+    p->gr = 0;
+    for (int gr : gr_opts) {
+        if (scan_layout(p->ng, gr, p->nksp, k, SCAN_RT).bytes <= LDS_LIMIT) {
+            p->gr = gr;
+            break;
+        }
+    }
+    p->lds_bytes = scan_layout(p->ng, p->gr, p->nksp, k, SCAN_RT).bytes;
     p->rt = SCAN_RT;
     const int bm = p->ng * 16;
     p->n_qt = B > 0 ? (B + bm - 1) / bm : 1;
@@ -986,7 +466,7 @@ int plan_knn(int B, int N, int d, int dtype, int k, int num_cu, KnnPlan *p)
     }
     p->rows_per_chunk = rpc;
     p->n_chunks = (int)(((long)N + rpc - 1) / rpc);
-    p->W = p->n_chunks * SCAN_WAVES;
+    p->W = p->n_chunks;
     if (p->W > MERGE_MAX_LISTS)
         return -1;
     // seed sample: about N/32 rows, 2048..32768, a multiple of 64 and at most N
@@ -1015,6 +495,13 @@ int plan_knn(int B, int N, int d, int dtype, int k, int num_cu, KnnPlan *p)
     off += align256((size_t)B * p->W * k * 4);
     p->off_cidx = off;
     off += align256((size_t)B * p->W * k * 4);
+    // candidate overflow: per scan wave, every (row, query) pair of one
+    // iteration beyond the LDS staging area
+    const long pairs = (long)SCAN_RT * 16 * p->ng * 16;
+    p->ovf_cap = pairs > STAGE_CAP ? (int)(pairs - STAGE_CAP) : 0;
+    p->grid = ((p->n_chunks + 7) / 8) * 8 * p->n_qt;
+    p->off_ovf = off;
+    off += align256((size_t)p->grid * SCAN_WAVES * 3 * (p->ovf_cap > 0 ? p->ovf_cap : 1) * 4);
     p->bytes = off;
     return 0;
 }
@@ -1088,17 +575,19 @@ hipError_t launch_knn(const KnnPlan &p, const void *queries, const void *bank,
     a.nksp = p.nksp;
     a.n_chunks = p.n_chunks;
     a.n_qt = p.n_qt;
-    a.W = p.W;
     a.rows_per_chunk = p.rows_per_chunk;
     a.tau = tau;
     a.ccnt = ccnt;
     a.ckey = ckey;
     a.cidx = cidx;
-    const int grid = ((p.n_chunks + 7) / 8) * 8 * p.n_qt;
+    a.ovf = (uint32_t *)(w + p.off_ovf);
+    a.ovf_cap = p.ovf_cap;
     const bool timed = t_scan_begin && t_scan_end;
     if (timed && (e = hipEventRecord(t_scan_begin, s)) != hipSuccess)
         return e;
-    e = p.dtype == 1 ? launch_scan_dt<1>(p, a, grid, s) : launch_scan_dt<0>(p, a, grid, s);
+    const bool ragged = p.d % (p.dtype == 1 ? 32 : 16) != 0;
+    e = p.dtype == 1 ? (ragged ? launch_scan_bf16_ragged(p, a, s) : launch_scan_bf16(p, a, s))
+                     : (ragged ? launch_scan_f32_ragged(p, a, s) : launch_scan_f32(p, a, s));
     if (e != hipSuccess)
         return e;
     if (timed && (e = hipEventRecord(t_scan_end, s)) != hipSuccess)

@@ -1,0 +1,11 @@
+// Bank-scan instantiations for fp32 embeddings, d a multiple of the 64-byte k-step.
+#include "scan.hpp"
+
+namespace rb {
+
+hipError_t launch_scan_f32(const KnnPlan &p, const ScanArgs &a, hipStream_t s)
+{
+    return launch_scan_r<0, false>(p, a, p.grid, s);
+}
+
+}  // namespace rb
