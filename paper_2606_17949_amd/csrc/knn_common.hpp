@@ -169,18 +169,6 @@ __device__ __forceinline__ uint64_t pack(uint32_t key, int32_t idx)
     return ((uint64_t)key << 32) | (uint32_t)idx;
 }
 
-__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v)
-{
-#pragma unroll
-    for (int m = 1; m < WAVE; m <<= 1) {
-        const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, m);
-        const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), m);
-        const uint64_t o = ((uint64_t)hi << 32) | lo;
-        v = o > v ? o : v;
-    }
-    return v;
-}
-
 // Inclusive prefix sum over the wave.
 __device__ __forceinline__ int wave_incl_scan(int v)
 {

@@ -182,35 +182,41 @@ __global__ __launch_bounds__(SCAN_THREADS, 1) void scan_kernel(const ScanArgs A)
         const float v = 0.5f * (qq - th);
         return v - ldexpf(fabsf(qq) + fabsf(th) + fabsf(v), -21);
     };
-    // Insert (key, idx) into the list of tile query i (wave-uniform call). The
-    // list always holds the k smallest (key, idx) pairs inserted so far: a new
-    // pair replaces the largest slot value by compare-and-swap, retried when
-    // another wave changed that slot in between (slot values only decrease, so
-    // a slot that still holds the observed maximum is still the maximum).
-    auto insert = [&](int i, uint32_t key, int32_t idx) {
-        if (key > bound_key(i))
-            return;
+    // Insert (key, idx) into the list of tile query i; every lane inserts its
+    // own candidate. The list always holds the k smallest (key, idx) pairs
+    // inserted so far: a new pair replaces the largest slot value by
+    // compare-and-swap, retried when another lane or wave changed that slot in
+    // between (slot values only decrease, so a slot that still holds the
+    // observed maximum is still the maximum). Lanes with nothing to insert
+    // pass pend = false.
+    auto insert_lanes = [&](bool pend, int i, uint32_t key, int32_t idx) {
         const uint64_t cand = pack(key, idx);
-        uint64_t *li = list + (size_t)i * k;
-        for (;;) {
-            const uint64_t v = lane < k ? lds_load64(li + lane) : 0;
-            const uint64_t m = wave_max_u64(v);
-            if (cand >= m)
-                return;
-            const uint64_t own = ballot(lane < k && v == m);
-            const int o = (int)__builtin_ctzll(own);
-            int ok = 0;
-            if (lane == o)
-                ok = lds_cas64(li + lane, m, cand);
-            if (__builtin_amdgcn_readlane(ok, o)) {
-                const uint64_t m2 = wave_max_u64(lane == o ? cand : v);
-                const uint32_t mk = (uint32_t)(m2 >> 32);
-                if (lane == 0) {
+        pend = pend && key <= bound_key(i);
+        const uint64_t *li = list + (size_t)i * k;
+        while (ballot(pend)) {
+            if (pend) {
+                uint64_t m = 0, m2 = 0;   // largest and second largest slot value
+                int mj = 0;
+                for (int j = 0; j < k; ++j) {
+                    const uint64_t v = lds_load64(li + j);
+                    if (v > m) {
+                        m2 = m;
+                        m = v;
+                        mj = j;
+                    } else if (v > m2) {
+                        m2 = v;
+                    }
+                }
+                if (cand >= m) {
+                    pend = false;
+                } else if (lds_cas64(const_cast<uint64_t *>(li) + mj, m, cand)) {
+                    // an upper bound of the list's new largest key
+                    const uint32_t mk = (uint32_t)((cand > m2 ? cand : m2) >> 32);
                     atomicMin(lmk_s + i, mk);
                     if (mk != KEY_NONE)
                         atomicMin(A.tau + q0 + i, mk);
+                    pend = false;
                 }
-                return;
             }
         }
     };
@@ -339,28 +345,22 @@ __global__ __launch_bounds__(SCAN_THREADS, 1) void scan_kernel(const ScanArgs A)
                 });
             });
         });
-        // Phase 2 (the accumulators are no longer needed): insert them in order.
-        if (nst > 0) {
-            const int nl = min(nst, STAGE_CAP);
-            for (int s = 0; s < nl; ++s) {
-                const int i = __builtin_amdgcn_readfirstlane(sq[s]);
-                const uint32_t key = (uint32_t)__builtin_amdgcn_readfirstlane((int)sk[s]);
-                const int32_t idx = __builtin_amdgcn_readfirstlane(si[s]);
-                insert(i, key, idx);
+        // Phase 2 (the accumulators are no longer needed): insert them, 64
+        // staged entries per round, one per lane.
+        for (int s0 = 0; s0 < nst; s0 += WAVE) {
+            const int s = s0 + lane;
+            int vi = 0, vx = 0;
+            uint32_t vk = 0;
+            if (s < min(nst, STAGE_CAP)) {
+                vi = sq[s];
+                vk = sk[s];
+                vx = si[s];
+            } else if (s < nst) {
+                vi = (int)ovf[s - STAGE_CAP];
+                vk = ovf[A.ovf_cap + s - STAGE_CAP];
+                vx = (int)ovf[2 * A.ovf_cap + s - STAGE_CAP];
             }
-            for (int s0 = STAGE_CAP; s0 < nst; s0 += WAVE) {
-                // 64 overflow entries per round: one load per lane, then lane by lane
-                const int s = s0 + lane;
-                const bool v = s < nst;
-                const int vi = v ? (int)ovf[s - STAGE_CAP] : 0;
-                const int vk = v ? (int)ovf[A.ovf_cap + s - STAGE_CAP] : 0;
-                const int vx = v ? (int)ovf[2 * A.ovf_cap + s - STAGE_CAP] : 0;
-                const int n = min(WAVE, nst - s0);
-                for (int j = 0; j < n; ++j)
-                    insert(__builtin_amdgcn_readlane(vi, j),
-                           (uint32_t)__builtin_amdgcn_readlane(vk, j),
-                           __builtin_amdgcn_readlane(vx, j));
-            }
+            insert_lanes(s < nst, vi, vk, vx);
         }
         // pick up bounds other workgroups have lowered
         for (int i = tid; i < BM; i += SCAN_THREADS)
