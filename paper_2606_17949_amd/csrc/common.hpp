@@ -47,35 +47,62 @@ __device__ __forceinline__ int lane_id() { return threadIdx.x & (WAVE - 1); }
 __device__ __forceinline__ float bf16lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
-// Wave-wide reductions: a butterfly inside each row of 16 lanes (quad
-// permutes, then half-row and row mirrors), then the row_bcast:15 and
+// Lane exchange by DPP: x of the lane that control CTRL names (rows outside
+// ROW_MASK keep their own x).
+template <int CTRL, int ROW_MASK = 0xf, typename T>
+__device__ __forceinline__ T dpp(T x)
+{
+    static_assert(sizeof(T) == 4, "32-bit values");
+    const int xi = __builtin_bit_cast(int, x);
+    return __builtin_bit_cast(T, __builtin_amdgcn_update_dpp(xi, xi, CTRL, ROW_MASK, 0xf, false));
+}
+
+// Butterfly inside each row of 16 lanes (quad permutes, then half-row and row
+// mirrors): every lane ends with its row's result.
+template <typename T, typename F>
+__device__ __forceinline__ T row16_reduce(T v, F op)
+{
+    v = op(v, dpp<0xb1>(v));    // quad_perm [1,0,3,2]
+    v = op(v, dpp<0x4e>(v));    // quad_perm [2,3,0,1]
+    v = op(v, dpp<0x141>(v));   // row_half_mirror
+    v = op(v, dpp<0x140>(v));   // row_mirror
+    return v;
+}
+
+// Wave-wide reductions: the row butterfly, then the row_bcast:15 and
 // row_bcast:31 steps carry rows 0..2 into row 3; lane 63 ends with the whole
 // wave's result, which is broadcast through a scalar register.
 template <typename T, typename F>
 __device__ __forceinline__ T wave_reduce(T v, F op)
 {
-    static_assert(sizeof(T) == 4, "32-bit values");
-    auto dpp = [](T x, int ctrl, int row_mask) -> T {
-        const int xi = __builtin_bit_cast(int, x);
-        int r;
-        switch (ctrl) {   // the control must be a compile-time constant
-        case 0xb1: r = __builtin_amdgcn_update_dpp(xi, xi, 0xb1, 0xf, 0xf, false); break;
-        case 0x4e: r = __builtin_amdgcn_update_dpp(xi, xi, 0x4e, 0xf, 0xf, false); break;
-        case 0x141: r = __builtin_amdgcn_update_dpp(xi, xi, 0x141, 0xf, 0xf, false); break;
-        case 0x140: r = __builtin_amdgcn_update_dpp(xi, xi, 0x140, 0xf, 0xf, false); break;
-        case 0x142: r = __builtin_amdgcn_update_dpp(xi, xi, 0x142, 0xa, 0xf, false); break;
-        default: r = __builtin_amdgcn_update_dpp(xi, xi, 0x143, 0xc, 0xf, false); break;
-        }
-        (void)row_mask;
-        return __builtin_bit_cast(T, r);
-    };
-    v = op(v, dpp(v, 0xb1, 0xf));    // quad_perm [1,0,3,2]
-    v = op(v, dpp(v, 0x4e, 0xf));    // quad_perm [2,3,0,1]
-    v = op(v, dpp(v, 0x141, 0xf));   // row_half_mirror
-    v = op(v, dpp(v, 0x140, 0xf));   // row_mirror: every lane holds its row's result
-    v = op(v, dpp(v, 0x142, 0xa));   // row_bcast:15 into rows 1 and 3
-    v = op(v, dpp(v, 0x143, 0xc));   // row_bcast:31 into rows 2 and 3
+    v = row16_reduce(v, op);
+    v = op(v, dpp<0x142, 0xa>(v));   // row_bcast:15 into rows 1 and 3
+    v = op(v, dpp<0x143, 0xc>(v));   // row_bcast:31 into rows 2 and 3
     return __builtin_bit_cast(T, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
+}
+
+// Lexicographic maximum of (hi, lo) pairs: over each row of 16 lanes when
+// WIDTH is 16 (every lane ends with its row's pair), over the wave when it is
+// 64 (broadcast to every lane).
+template <int WIDTH>
+__device__ __forceinline__ void reduce_max_pair(uint32_t &hi, uint32_t &lo)
+{
+    auto step = [&](uint32_t oh, uint32_t ol) {
+        // one 64-bit compare, two selects (no branches)
+        const bool take = (((uint64_t)oh << 32) | ol) > (((uint64_t)hi << 32) | lo);
+        hi = take ? oh : hi;
+        lo = take ? ol : lo;
+    };
+    step(dpp<0xb1>(hi), dpp<0xb1>(lo));
+    step(dpp<0x4e>(hi), dpp<0x4e>(lo));
+    step(dpp<0x141>(hi), dpp<0x141>(lo));
+    step(dpp<0x140>(hi), dpp<0x140>(lo));
+    if constexpr (WIDTH == 64) {
+        step(dpp<0x142, 0xa>(hi), dpp<0x142, 0xa>(lo));
+        step(dpp<0x143, 0xc>(hi), dpp<0x143, 0xc>(lo));
+        hi = (uint32_t)__builtin_amdgcn_readlane((int)hi, 63);
+        lo = (uint32_t)__builtin_amdgcn_readlane((int)lo, 63);
+    }
 }
 
 template <typename F>

@@ -83,28 +83,38 @@ __global__ __launch_bounds__(256) void score_kernel(const float *__restrict__ q_
 // Greedy assignment. Wave 0 runs the sequential loop over requests; waves
 // 1..15 fill, one chunk of requests ahead, an LDS double buffer with what does
 // not depend on the state: per (request, instance) the base score and the
-// predicted output length on the instance's model. Instance i = lane + 64*u
-// lives in register slot u of wave 0's lane, with its state. Per request: the
-// latency maximum (one wave reduction), the scores, the largest score (one
-// wave reduction) and the lowest index holding it (a ballot), then the owner
-// lane updates the chosen instance.
+// predicted output length on the instance's model. WIDTH = 16 (I <= 16):
+// instance i = lane % 16, replicated in the four rows of 16 lanes, so every
+// reduction stays inside a row and leaves its result in every lane. WIDTH = 64:
+// instance i = lane + 64*u in register slot u. Per request: the latency
+// maximum (one reduction), the scores, then one reduction of (score key,
+// ~instance) pairs that yields the largest score and, among equal scores, the
+// lowest instance index; the lanes holding that instance update its state.
 constexpr int ASSIGN_THREADS = 1024;
 constexpr int ASSIGN_WAVES = ASSIGN_THREADS / WAVE;
 constexpr int ASSIGN_LDS_FLOATS = 8192;   // per buffer: chunk rows x instances x 2
 
-template <int IPL>
+template <int IPL, int WIDTH>
 __global__ __launch_bounds__(ASSIGN_THREADS) void assign_kernel(
     const float *__restrict__ q_hat, const float *__restrict__ l_hat,
     const int32_t *__restrict__ plen, int B, int M, const InstArgs in, int I, float wq, float wl,
     float wc, int32_t *__restrict__ assign, float *__restrict__ chosen)
 {
-    constexpr int IP = IPL * WAVE;                        // padded instance count
+    static_assert(WIDTH == 64 || IPL == 1, "a 16-lane row holds one slot");
+    constexpr int IP = IPL * WIDTH;                       // instances per LDS row
     constexpr int CH = ASSIGN_LDS_FLOATS / (2 * IP);      // requests per chunk
     __shared__ float base_s[2][CH][IP];
     __shared__ float lv_s[2][CH][IP];
     __shared__ float l_s[2][CH];
     const int lane = lane_id(), wave = threadIdx.x >> 6;
     const int n_ch = (B + CH - 1) / CH;
+    auto inst = [&](int u) { return WIDTH == 16 ? (lane & 15) : lane + WAVE * u; };
+    auto fmax_all = [&](float v) {
+        if constexpr (WIDTH == 16)
+            return row16_reduce(v, [](float x, float y) { return fmaxf(x, y); });
+        else
+            return wave_max(v);
+    };
 
     // producers: request r of chunk c into buffer c & 1, one wave per request
     auto produce = [&](int c) {
@@ -120,7 +130,7 @@ __global__ __launch_bounds__(ASSIGN_THREADS) void assign_kernel(
             float cmax = -INFINITY;
 #pragma unroll
             for (int u = 0; u < IPL; ++u) {
-                const int i = lane + WAVE * u;
+                const int i = inst(u);
                 const int m = i < I ? in.model[i] : -1;
                 const bool ok = (unsigned)m < (unsigned)M;
                 qv[u] = ok ? qr[m] : 0.f;
@@ -129,11 +139,13 @@ __global__ __launch_bounds__(ASSIGN_THREADS) void assign_kernel(
                 if (ok)
                     cmax = fmaxf(cmax, C[u]);
             }
-            cmax = wave_max(cmax);
+            cmax = fmax_all(cmax);
+            if (lane < (WIDTH == 16 ? 16 : WAVE)) {
 #pragma unroll
-            for (int u = 0; u < IPL; ++u) {
-                base_s[buf][j][lane + WAVE * u] = base_score(qv[u], C[u], cmax, wq, wc);
-                lv_s[buf][j][lane + WAVE * u] = lv[u];
+                for (int u = 0; u < IPL; ++u) {
+                    base_s[buf][j][lane + WAVE * u] = base_score(qv[u], C[u], cmax, wq, wc);
+                    lv_s[buf][j][lane + WAVE * u] = lv[u];
+                }
             }
             if (lane == 0)
                 l_s[buf][j] = l;
@@ -152,11 +164,12 @@ __global__ __launch_bounds__(ASSIGN_THREADS) void assign_kernel(
     }
 
     // consumer: instance state in registers
+    const int col = WIDTH == 16 ? (lane & 15) : lane;   // this lane's column of an LDS row
     float p[IPL], a[IPL], rP[IPL], rD[IPL];
     bool valid[IPL];
 #pragma unroll
     for (int u = 0; u < IPL; ++u) {
-        const int i = lane + WAVE * u;
+        const int i = inst(u);
         // an instance whose model id is outside [0, M) is never chosen
         const int m = i < I ? in.model[i] : -1;
         valid[u] = (unsigned)m < (unsigned)M;
@@ -172,8 +185,8 @@ __global__ __launch_bounds__(ASSIGN_THREADS) void assign_kernel(
         float l = l_s[buf][0], bs[IPL], lv[IPL];
 #pragma unroll
         for (int u = 0; u < IPL; ++u) {
-            bs[u] = base_s[buf][0][lane + WAVE * u];
-            lv[u] = lv_s[buf][0][lane + WAVE * u];
+            bs[u] = base_s[buf][0][col + WAVE * u];
+            lv[u] = lv_s[buf][0][col + WAVE * u];
         }
         for (int j = 0; j < rows; ++j) {
             const int r = c * CH + j;
@@ -183,8 +196,8 @@ __global__ __launch_bounds__(ASSIGN_THREADS) void assign_kernel(
             float bsn[IPL], lvn[IPL];
 #pragma unroll
             for (int u = 0; u < IPL; ++u) {
-                bsn[u] = base_s[buf][jn][lane + WAVE * u];
-                lvn[u] = lv_s[buf][jn][lane + WAVE * u];
+                bsn[u] = base_s[buf][jn][col + WAVE * u];
+                lvn[u] = lv_s[buf][jn][col + WAVE * u];
             }
             float T[IPL];
             float tmax = -INFINITY;
@@ -194,7 +207,7 @@ __global__ __launch_bounds__(ASSIGN_THREADS) void assign_kernel(
                 if (valid[u])
                     tmax = fmaxf(tmax, T[u]);
             }
-            tmax = wave_max(tmax);
+            tmax = fmax_all(tmax);
             uint32_t best = 0;   // f2key of this lane's best score (0 = no candidate)
             int bu = 0;
 #pragma unroll
@@ -206,25 +219,20 @@ __global__ __launch_bounds__(ASSIGN_THREADS) void assign_kernel(
                     bu = u;
                 }
             }
-            // largest score, then the lowest instance index holding it
-            const uint32_t kmax = wave_max_u32(best);
-            const uint32_t mine = (best == kmax && kmax != 0) ? (uint32_t)(lane + WAVE * bu) : ~0u;
-            const uint32_t imin = wave_min_u32(mine);
-            const bool found = kmax != 0;
-            const int istar = found ? (int)imin : 0;
-            const int wl_lane = istar & (WAVE - 1), wu = istar / WAVE;
+            uint32_t hi = best, lo = best ? ~(uint32_t)inst(bu) : 0u;
+            reduce_max_pair<WIDTH>(hi, lo);
+            const bool found = hi != 0;
+            const int istar = found ? (int)~lo : 0;
             if (lane == 0) {
                 assign[r] = istar;
                 if (chosen)
-                    chosen[r] = found ? key2f(kmax) : __builtin_nanf("");
+                    chosen[r] = found ? key2f(hi) : __builtin_nanf("");
             }
-            if (found && lane == wl_lane) {
 #pragma unroll
-                for (int u = 0; u < IPL; ++u) {
-                    if (u == wu) {
-                        p[u] += l;
-                        a[u] += lv[u];
-                    }
+            for (int u = 0; u < IPL; ++u) {
+                if (found && inst(u) == istar) {
+                    p[u] += l;
+                    a[u] += lv[u];
                 }
             }
             l = ln;
@@ -238,8 +246,8 @@ __global__ __launch_bounds__(ASSIGN_THREADS) void assign_kernel(
     }
 #pragma unroll
     for (int u = 0; u < IPL; ++u) {
-        const int i = lane + WAVE * u;
-        if (i < I && valid[u]) {
+        const int i = inst(u);
+        if (lane < (WIDTH == 16 ? 16 : WAVE) && i < I && valid[u]) {
             in.p[i] = p[u];
             in.a[i] = a[u];
         }
@@ -271,14 +279,15 @@ hipError_t launch_assign(const float *q_hat, const float *l_hat, const int32_t *
                          int32_t *assign, float *chosen, hipStream_t s)
 {
     const int ipl = (I + WAVE - 1) / WAVE;
-#define RB_ASSIGN(N)                                                                             \
-    hipLaunchKernelGGL(assign_kernel<N>, dim3(1), dim3(ASSIGN_THREADS), 0, s, q_hat, l_hat,      \
+#define RB_ASSIGN(N, W)                                                                          \
+    hipLaunchKernelGGL((assign_kernel<N, W>), dim3(1), dim3(ASSIGN_THREADS), 0, s, q_hat, l_hat, \
                        plen, B, M, in, I, wq, wl, wc, assign, chosen)
-    if (ipl <= 1) RB_ASSIGN(1);
-    else if (ipl <= 2) RB_ASSIGN(2);
-    else if (ipl <= 4) RB_ASSIGN(4);
-    else if (ipl <= 8) RB_ASSIGN(8);
-    else if (ipl <= 16) RB_ASSIGN(16);
+    if (I <= 16) RB_ASSIGN(1, 16);
+    else if (ipl <= 1) RB_ASSIGN(1, 64);
+    else if (ipl <= 2) RB_ASSIGN(2, 64);
+    else if (ipl <= 4) RB_ASSIGN(4, 64);
+    else if (ipl <= 8) RB_ASSIGN(8, 64);
+    else if (ipl <= 16) RB_ASSIGN(16, 64);
     else return hipErrorInvalidValue;
 #undef RB_ASSIGN
     return hipGetLastError();

@@ -150,6 +150,8 @@ ROUTE_CASES = [
     (33, 16, 512),
     (7, 3, 1024),     # largest instance count
     (300, 4, 65),     # I just past one wave's lanes
+    (40, 4, 16),      # the most instances one 16-lane row holds
+    (40, 4, 17),      # one more: a full-wave layout
 ]
 
 
