@@ -18,11 +18,11 @@ constexpr int MERGE_THREADS = 256;  // one query per workgroup
 constexpr int MERGE_CAP = 4096;     // candidates per query the merge holds in LDS
 constexpr int MERGE_MAX_LISTS = MERGE_THREADS * 16;
 constexpr int RB_MAX_K_DEV = 64;    // largest k (the ABI limit)
-constexpr int SEED_MAX_GROUPS = 2048;
+constexpr int SEED_MAX_GROUPS = 512;   // S / 64 for S <= 32768
 
 // How one rb_knn_topk call is split.
 //  * seed: S bank rows spread evenly over the bank; per query, the k-th
-//    smallest of the S/16 minima over groups of 16 of them bounds the k-th
+//    smallest of the S/64 minima over groups of 64 of them bounds the k-th
 //    nearest distance from above (k distinct rows lie at or below it).
 //  * scan: query tiles of 16*ng queries, whose first gr groups stay in LDS
 //    for the whole call while the others stream through it; the

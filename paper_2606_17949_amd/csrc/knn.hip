@@ -3,7 +3,7 @@
 //
 // Kernels of one call:
 //   seed_groups_kernel  distances of every query to S bank rows spread evenly
-//                       over the bank; minima over groups of 16 of those rows
+//                       over the bank; minima over groups of 64 of those rows
 //   seed_bound_kernel   per query: |q|^2, and the k-th smallest group minimum
 //                       as the starting bound of the k-th nearest distance
 //   scan_kernel         the bank once through MFMA (scan.hpp): one workgroup
@@ -63,43 +63,61 @@ __device__ __forceinline__ long seed_row(int j, int N, int S)
     return (long)j * N / S;
 }
 
-// One wave per (query group of 16, block of 64 sample rows): partial distances
-// p = |x|^2 - 2<q,x> by MFMA, then each lane's minimum over its 16 rows. The
-// 16 waves of a workgroup take 16 query groups of the same sample block, so
-// the block's rows are fetched once into the compute unit's caches.
+// One workgroup of 16 waves per group of 64 sample rows; wave w takes query
+// group 16*blockIdx.y + w. Per k-step the 64 rows' 64-byte slices are staged
+// once in an LDS double buffer (one 16-byte load by each of 256 threads), so
+// the 16 waves do not each fetch them; each wave reads the 4 row-tile
+// fragments from LDS and its own query fragment (loaded a k-step ahead) from
+// global memory. p = |x|^2 - 2<q,x> by MFMA; each query keeps the minimum over
+// the 64 rows.
 constexpr int SEED_WAVES = 16;
 
 template <int DT>
 __global__ __launch_bounds__(SEED_WAVES * WAVE) void seed_groups_kernel(const SeedArgs A)
 {
     constexpr int VEC = Elem<DT>::VEC, ESZ = Elem<DT>::ESZ;
-    const int lane = lane_id(), col = lane & 15, jg = lane >> 4;
+    __shared__ i32x4 abuf[2][4][WAVE];   // [buffer][row tile][lane]
+    const int tid = threadIdx.x, lane = lane_id(), wave = tid >> 6;
+    const int col = lane & 15, jg = lane >> 4;
     const int sb = blockIdx.x;
-    const int qg = blockIdx.y * SEED_WAVES + (threadIdx.x >> 6);
-    if (qg >= A.n_qg)
-        return;
+    const int qg = blockIdx.y * SEED_WAVES + wave;
+    const bool wv = qg < A.n_qg;
     const size_t rowb = (size_t)A.d * ESZ;
     const int q = qg * 16 + col;
-    const bool qv = q < A.B;
+    const bool qv = wv && q < A.B;
+    const i32x4 z = {0, 0, 0, 0};
+    // staging: thread tid < 256 loads row tile tid/64, lane tid%64 of every k-step
+    const int st_t = (tid >> 6) & 3, st_l = tid & 63;
+    const uint8_t *sp = A.bank + (size_t)seed_row(sb * 64 + st_t * 16 + (st_l & 15), A.N, A.S) * rowb +
+                        (st_l >> 4) * 16;
+    auto stage_load = [&](int s) -> i32x4 {
+        return s * 4 * VEC + (st_l >> 4) * VEC < A.d ? load16(sp + (size_t)s * KSTEP_BYTES) : z;
+    };
     const uint8_t *qp = A.queries + (qv ? (size_t)q * rowb : 0) + jg * 16;
-    const uint8_t *ap[4];
+    auto query_load = [&](int s) -> i32x4 {
+        return qv && s * 4 * VEC + jg * VEC < A.d ? load16(qp + (size_t)s * KSTEP_BYTES) : z;
+    };
     f32x4 acc[4];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-        ap[t] = A.bank + (size_t)seed_row(sb * 64 + t * 16 + col, A.N, A.S) * rowb + jg * 16;
+    for (int t = 0; t < 4; ++t)
 #pragma unroll
         for (int e = 0; e < 4; ++e)
             acc[t][e] = -0.5f * A.bank_norms[seed_row(sb * 64 + t * 16 + jg * 4 + e, A.N, A.S)];
-    }
+    if (tid < 256)
+        abuf[0][st_t][st_l] = stage_load(0);
+    i32x4 b = query_load(0);
+    __syncthreads();
     for (int s = 0; s < A.nks; ++s) {
-        const bool kv = s * 4 * VEC + jg * VEC < A.d;
-        const i32x4 z = {0, 0, 0, 0};
-        const i32x4 b = kv && qv ? load16(qp + (size_t)s * KSTEP_BYTES) : z;
+        const bool more = s + 1 < A.nks;
+        const i32x4 an = tid < 256 && more ? stage_load(s + 1) : z;
+        const i32x4 bn = more ? query_load(s + 1) : z;
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
-            const i32x4 a = kv ? load16(ap[t] + (size_t)s * KSTEP_BYTES) : z;
-            acc[t] = mfma_step<DT>(a, b, acc[t]);
-        }
+        for (int t = 0; t < 4; ++t)
+            acc[t] = mfma_step<DT>(abuf[s & 1][t][lane], b, acc[t]);
+        if (tid < 256 && more)
+            abuf[(s + 1) & 1][st_t][st_l] = an;
+        b = bn;
+        __syncthreads();
     }
     float m = INFINITY;
 #pragma unroll
@@ -107,8 +125,11 @@ __global__ __launch_bounds__(SEED_WAVES * WAVE) void seed_groups_kernel(const Se
 #pragma unroll
         for (int e = 0; e < 4; ++e)
             m = fminf(m, -2.f * acc[t][e]);
-    if (qv)
-        A.gmin[(size_t)q * A.G + sb * 4 + jg] = m;
+    // lanes col, col+16, col+32, col+48 hold the four row quarters of one query
+    m = fminf(m, __shfl_xor(m, 16));
+    m = fminf(m, __shfl_xor(m, 32));
+    if (qv && jg == 0)
+        A.gmin[(size_t)q * A.G + sb] = m;
 }
 
 // One wave per query: |q|^2, and the starting bound = |q|^2 + the k-th smallest
@@ -392,12 +413,8 @@ hipError_t launch_seed_bound(const KnnPlan &p, const void *queries, const float 
     const int grid = (p.B + 3) / 4;
     const uint8_t *q = (const uint8_t *)queries;
     const int G = p.S ? p.G : 0;
-    if (G <= 1024)
-        hipLaunchKernelGGL((seed_bound_kernel<DT, 16>), dim3(grid), dim3(256), 0, s, q, p.B, p.d,
-                           p.k, gmin, G, qn, tau);
-    else
-        hipLaunchKernelGGL((seed_bound_kernel<DT, 32>), dim3(grid), dim3(256), 0, s, q, p.B, p.d,
-                           p.k, gmin, G, qn, tau);
+    hipLaunchKernelGGL((seed_bound_kernel<DT, SEED_MAX_GROUPS / WAVE>), dim3(grid), dim3(256), 0, s,
+                       q, p.B, p.d, p.k, gmin, G, qn, tau);
     return hipGetLastError();
 }
 
@@ -478,10 +495,10 @@ int plan_knn(int B, int N, int d, int dtype, int k, int num_cu, KnnPlan *p)
     if (S > N)
         S = N;
     S = S / 64 * 64;
-    if (S / 16 < k)
+    if (S / 64 < k)
         S = 0;
     p->S = (int)S;
-    p->G = (int)(S / 16);
+    p->G = (int)(S / 64);
     size_t off = 0;
     p->off_tau = off;
     off += align256((size_t)B * 4);
