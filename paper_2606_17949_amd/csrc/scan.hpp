@@ -173,14 +173,11 @@ __global__ __launch_bounds__(SCAN_THREADS, 1) void scan_kernel(const ScanArgs A)
     // Filter threshold of tile query i: a value is a candidate if acc >= nu (a
     // superset of distance <= the bound; the exact test follows on insertion).
     auto nu_of = [&](int i) -> float {
-        if (q0 + i >= A.B)
-            return INFINITY;
         const uint32_t tk = bound_key(i);
-        if (tk == KEY_NONE)
-            return -FLT_MAX;
         const float qq = qn_s[i], th = key2f(tk);
         const float v = 0.5f * (qq - th);
-        return v - ldexpf(fabsf(qq) + fabsf(th) + fabsf(v), -21);
+        const float nu = v - ldexpf(fabsf(qq) + fabsf(th) + fabsf(v), -21);
+        return q0 + i >= A.B ? INFINITY : tk == KEY_NONE ? -FLT_MAX : nu;
     };
     // Insert (key, idx) into the list of tile query i; every lane inserts its
     // own candidate. The list always holds the k smallest (key, idx) pairs
@@ -306,18 +303,32 @@ __global__ __launch_bounds__(SCAN_THREADS, 1) void scan_kernel(const ScanArgs A)
         const long wr0 = rbeg + (long)it * RWG + wave * RW;
         uint32_t *ovf = A.ovf + (size_t)(blockIdx.x * SCAN_WAVES + wave) * 3 * A.ovf_cap;
         int nst = 0;
+        // One test per group over its RT*4 accumulators, four groups at a time
+        // so that their threshold reads from LDS overlap; then staging for the
+        // groups with a hit.
+        constexpr int TB = NG < 4 ? NG : 4;
+        uint32_t hits = 0;
+        static_for<0, NG / TB>([&](auto GB) {
+            constexpr int g0 = decltype(GB)::value * TB;
+            float nus[TB];
+            static_for<0, TB>([&](auto G) { nus[G.value] = nu_of((g0 + G.value) * 16 + col); });
+            static_for<0, TB>([&](auto G) {
+                constexpr int g = g0 + decltype(G)::value;
+                float m = -INFINITY;
+                static_for<0, RT>([&](auto TT) {
+                    constexpr int tt = decltype(TT)::value;
+                    m = fmaxf(m, fmaxf(fmaxf(acc[tt][g][0], acc[tt][g][1]),
+                                       fmaxf(acc[tt][g][2], acc[tt][g][3])));
+                });
+                hits |= ballot(m >= nus[G.value]) ? 1u << g : 0u;
+            });
+        });
         static_for<0, NG>([&](auto G) {
             constexpr int g = decltype(G)::value;
+            if (!(hits >> g & 1u))
+                return;
             const int i = g * 16 + col;
             const float nu = nu_of(i);
-            float m = -INFINITY;
-            static_for<0, RT>([&](auto TT) {
-                constexpr int tt = decltype(TT)::value;
-                m = fmaxf(m, fmaxf(fmaxf(acc[tt][g][0], acc[tt][g][1]),
-                                   fmaxf(acc[tt][g][2], acc[tt][g][3])));
-            });
-            if (!ballot(m >= nu))
-                return;
             const float qq = qn_s[i];
             static_for<0, RT>([&](auto TT) {
                 constexpr int tt = decltype(TT)::value;
