@@ -32,6 +32,38 @@ BF16_PEAK_TFLOPS = 2500.0      # dense bf16 MFMA
 FP32_PEAK_TFLOPS = 157.3
 
 
+# Sources the scan kernel is built from: measured traffic is reported only for
+# the build whose sources it was taken with.
+SCAN_SOURCES = ["paper_2606_17949_amd/csrc/scan.hpp", "paper_2606_17949_amd/csrc/knn_common.hpp",
+                "paper_2606_17949_amd/csrc/kernels.hpp", "paper_2606_17949_amd/csrc/common.hpp"]
+TRAFFIC_FILE = "profiles/scan_traffic.json"
+
+
+def scan_source_digest():
+    import hashlib
+    h = hashlib.sha256()
+    root = os.path.dirname(os.path.abspath(__file__))
+    for rel in SCAN_SOURCES:
+        with open(os.path.join(root, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload):
+    """HBM bytes per scan launch from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE
+    passes (scaled by the copy calibration), or None when they were taken on other
+    sources or another workload."""
+    root = os.path.dirname(os.path.abspath(__file__))
+    try:
+        with open(os.path.join(root, TRAFFIC_FILE)) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("sources_sha256") != scan_source_digest() or t.get("workload") != workload:
+        return None
+    return t.get("bytes_per_launch")
+
+
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
@@ -45,6 +77,10 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=0,
                     help="requests in the CPU oracle sample (0: 8 per host thread)")
+    ap.add_argument("--record-traffic", metavar="PMC_DIR",
+                    help="turn rocprofv3 FETCH_SIZE/WRITE_SIZE passes over the scan (PMC_DIR/fetch, "
+                         "PMC_DIR/write) and over --calibrate-copy (PMC_DIR/copyfetch, "
+                         "PMC_DIR/copywrite) into PMC_DIR/scan_traffic.json for --workload")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain device copy of 1 GiB (counter calibration)")
     return ap.parse_args()
@@ -62,8 +98,44 @@ def calibrate_copy():
     print(json.dumps({"calibrate_copy_bytes": n, "launches": 3}), flush=True)
 
 
+def _counter_means(path, kernel_sub, counter):
+    import csv
+    import glob
+    vals = []
+    for f in glob.glob(os.path.join(path, "**", "*counter_collection.csv"), recursive=True):
+        with open(f) as fh:
+            for r in csv.DictReader(fh):
+                if kernel_sub in r["Kernel_Name"] and r["Counter_Name"] == counter:
+                    vals.append(float(r["Counter_Value"]))
+    if not vals:
+        raise SystemExit(f"no {counter} values for {kernel_sub} under {path}")
+    return sum(vals) / len(vals), len(vals)
+
+
+def record_traffic(pmc, workload):
+    """Scan HBM bytes per launch: counter KiB x (bytes a 1 GiB copy moves / the
+    same counter's KiB for that copy)."""
+    copy_bytes = float(1 << 30)
+    cf, _ = _counter_means(os.path.join(pmc, "copyfetch"), "copyBuffer", "FETCH_SIZE")
+    cw, _ = _counter_means(os.path.join(pmc, "copywrite"), "copyBuffer", "WRITE_SIZE")
+    sf, nf = _counter_means(os.path.join(pmc, "fetch"), "scan_kernel", "FETCH_SIZE")
+    sw, nw = _counter_means(os.path.join(pmc, "write"), "scan_kernel", "WRITE_SIZE")
+    kf, kw = copy_bytes / cf, copy_bytes / cw     # bytes per counter unit
+    out = {"workload": workload, "sources_sha256": scan_source_digest(),
+           "fetch_size_kib": round(sf, 1), "write_size_kib": round(sw, 1), "dispatches": [nf, nw],
+           "copy_fetch_kib_per_gib": round(cf, 1), "copy_write_kib_per_gib": round(cw, 1),
+           "fetch_bytes": round(sf * kf), "write_bytes": round(sw * kw),
+           "bytes_per_launch": round(sf * kf + sw * kw)}
+    with open(os.path.join(pmc, "scan_traffic.json"), "w") as f:
+        json.dump(out, f, indent=1)
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
+    if args.record_traffic:
+        record_traffic(args.record_traffic, args.workload)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               "(the bank-sharded multi-GPU design is described in DESIGN.md).", file=sys.stderr)
@@ -148,11 +220,12 @@ def main():
     ridge = peak_tf * 1e12 / (HBM_PEAK_GBS * 1e9)
     if ai < ridge:
         roof = {"bound": "hbm", "achieved": round(scan_gbs, 1), "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": round(scan_gbs / HBM_PEAK_GBS, 4), "traffic": None}
+                "unit": "GB/s", "frac": round(scan_gbs / HBM_PEAK_GBS, 4),
+                "traffic": measured_traffic(cfg.name)}
     else:
         tf = flops / (scan_avg / 1e3) / 1e12
         roof = {"bound": "mfma", "achieved": round(tf, 1), "peak": peak_tf, "unit": "TFLOP/s",
-                "frac": round(tf / peak_tf, 4), "traffic": None}
+                "frac": round(tf / peak_tf, 4), "traffic": measured_traffic(cfg.name)}
     roof["kernel"] = "scan_kernel (bank distance contraction + fused per-chunk top-k)"
     roof["per_launch"] = {"bytes": bank_bytes, "flops": flops, "avg_us": round(scan_avg * 1e3, 2),
                           "p10_us": round(float(np.percentile(scan_ms, 10)) * 1e3, 2),
