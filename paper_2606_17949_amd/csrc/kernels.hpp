@@ -14,9 +14,9 @@ constexpr int SCAN_PREFETCH = 3;    // k-steps whose loads are in flight ahead o
 constexpr int SCAN_UNROLL = 4;      // register ring of bank fragments; k-steps are padded to it
 constexpr int STAGE_CAP = 256;      // per-wave LDS staging of one iteration's candidates
 constexpr size_t LDS_LIMIT = 160 * 1024;
-constexpr int MERGE_THREADS = 256;  // one query per workgroup
-constexpr int MERGE_CAP = 4096;     // candidates per query the merge holds in LDS
-constexpr int MERGE_MAX_LISTS = MERGE_THREADS * 16;
+constexpr int MERGE_WAVES = 4;      // queries per merge workgroup, one wave each
+constexpr int MERGE_CAP = 2048;     // candidates per query the merge holds in LDS
+constexpr int MERGE_MAX_LISTS = 64 * 64;   // 64 lists per lane
 constexpr int RB_MAX_K_DEV = 64;    // largest k (the ABI limit)
 constexpr int SEED_MAX_GROUPS = 512;   // S / 64 for S <= 32768
 

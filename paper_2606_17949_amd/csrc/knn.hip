@@ -196,180 +196,124 @@ struct MergeArgs {
 
 // The label gather and average: sum over neighbours j = 0..k-1 in order. A
 // neighbour index outside [0, N) makes both averages NaN instead of reading
-// out of bounds.
+// out of bounds (the check does not end the loop, so the k loads can all be
+// in flight together).
 __device__ __forceinline__ void average_labels(const int32_t *nbr, int k, const float *qual,
                                                const float *len, int N, int M, int m,
                                                float *q_out, float *l_out)
 {
     float sq = 0.f, sl = 0.f;
+    bool bad = false;
+#pragma unroll 8
     for (int j = 0; j < k; ++j) {
         const int32_t n = nbr[j];
-        if (n < 0 || n >= N) {
-            sq = sl = __builtin_nanf("");
-            break;
-        }
-        const size_t o = (size_t)n * M + m;
+        const bool ok = n >= 0 && n < N;
+        bad |= !ok;
+        const size_t o = (size_t)(ok ? n : 0) * M + m;
         sq += qual[o];
         sl += len[o];
     }
-    *q_out = sq / (float)k;
-    *l_out = sl / (float)k;
+    *q_out = bad ? __builtin_nanf("") : sq / (float)k;
+    *l_out = bad ? __builtin_nanf("") : sl / (float)k;
 }
 
-// One workgroup per query: gather the non-empty lists' entries into LDS (a
-// block-wide prefix sum places them), select the k smallest (key, index) pairs
-// bit by bit from the most significant key bit, order them, then gather and
-// average the labels. Entries that do not fit in LDS are read from the
-// workspace instead (slower, same result).
-template <int LPT, bool PREDICT>
-__global__ __launch_bounds__(MERGE_THREADS) void merge_kernel(const MergeArgs A)
+// One wave per query (MERGE_WAVES queries per workgroup, no workgroup
+// barrier): the wave's lanes take the lists w = lane + 64*u, a wave prefix
+// sum places their entries as packed (key << 32 | index) values in LDS, then
+// k rounds each pick the smallest entry above the previous pick (one pass
+// over the entries and one 64-bit wave minimum; entries are distinct, so the
+// picks are the k smallest in order). Lane r ends with pick r. Entries that do
+// not fit in LDS are read from the workspace in every round instead (slower,
+// same result). Then, optionally, the label gather and average.
+template <int LPL, bool PREDICT>
+__global__ __launch_bounds__(MERGE_WAVES * WAVE) void merge_kernel(const MergeArgs A)
 {
-    __shared__ uint32_t ek[MERGE_CAP];
-    __shared__ int32_t ei[MERGE_CAP];
-    __shared__ int wsum[MERGE_THREADS / WAVE];
-    __shared__ int red[2][MERGE_THREADS / WAVE];
-    __shared__ uint32_t sk[RB_MAX_K_DEV];
-    __shared__ int32_t si[RB_MAX_K_DEV];
-    __shared__ int32_t so[RB_MAX_K_DEV];
-    __shared__ int ns_s;
-    const int tid = threadIdx.x, lane = lane_id(), wave = tid >> 6;
-    const int b = blockIdx.x;
+    __shared__ uint64_t ent_all[MERGE_WAVES][MERGE_CAP];
+    const int lane = lane_id(), wave = threadIdx.x >> 6;
+    const int b = blockIdx.x * MERGE_WAVES + wave;
+    if (b >= A.B)
+        return;
+    uint64_t *ent = ent_all[wave];
     const int k = A.k, W = A.W;
     const int32_t *cnt = A.ccnt + (size_t)b * W;
     const size_t base = (size_t)b * W * k;
-
-    // lists w = tid + MERGE_THREADS*u of this thread, their lengths and offsets
-    int n[LPT], mine = 0;
+    int n[LPL], mine = 0;
 #pragma unroll
-    for (int u = 0; u < LPT; ++u) {
-        const int w = tid + MERGE_THREADS * u;
+    for (int u = 0; u < LPL; ++u) {
+        const int w = lane + WAVE * u;
         n[u] = w < W ? cnt[w] : 0;
         mine += n[u];
     }
-    float incl = (float)mine;   // block prefix sum (counts < 2^24, exact in fp32)
-#pragma unroll
-    for (int m = 1; m < WAVE; m <<= 1) {
-        const float o = __shfl_up(incl, m);
-        if (lane >= m)
-            incl += o;
-    }
-    if (lane == WAVE - 1)
-        wsum[wave] = (int)incl;
-    if (tid == 0)
-        ns_s = 0;
-    __syncthreads();
-    int off = (int)incl - mine, total = 0;
-    for (int w = 0; w < MERGE_THREADS / WAVE; ++w) {
-        off += w < wave ? wsum[w] : 0;
-        total += wsum[w];
-    }
+    const int incl = wave_incl_scan(mine);
+    const int total = __builtin_amdgcn_readlane(incl, WAVE - 1);
     const bool in_lds = total <= MERGE_CAP;
     if (in_lds) {
+        // the first GE entries of every list of this lane are loaded together
+        // (lists are short once the bound is tight); longer lists finish after
+        constexpr int GE = LPL <= 8 ? 4 : 1;
+        int off = incl - mine;
+        uint32_t kk[LPL][GE];
+        int32_t ii[LPL][GE];
 #pragma unroll
-        for (int u = 0; u < LPT; ++u) {
-            const size_t o = base + (size_t)(tid + MERGE_THREADS * u) * k;
-            for (int j = 0; j < n[u]; ++j) {
-                ek[off + j] = A.ckey[o + j];
-                ei[off + j] = A.cidx[o + j];
+        for (int u = 0; u < LPL; ++u) {
+            const size_t o = base + (size_t)(lane + WAVE * u) * k;
+#pragma unroll
+            for (int j = 0; j < GE; ++j) {
+                kk[u][j] = j < n[u] ? A.ckey[o + j] : 0u;
+                ii[u][j] = j < n[u] ? A.cidx[o + j] : 0;
             }
+        }
+#pragma unroll
+        for (int u = 0; u < LPL; ++u) {
+            const size_t o = base + (size_t)(lane + WAVE * u) * k;
+#pragma unroll
+            for (int j = 0; j < GE; ++j)
+                if (j < n[u])
+                    ent[off + j] = pack(kk[u][j], ii[u][j]);
+            for (int j = GE; j < n[u]; ++j)
+                ent[off + j] = pack(A.ckey[o + j], A.cidx[o + j]);
             off += n[u];
         }
     }
-    __syncthreads();
-
-    int phase = 0;
-    auto block_sum = [&](int c) -> int {
-        const float sw = wave_sum((float)c);
-        int *slot = red[phase & 1];
-        if (lane == 0)
-            slot[wave] = (int)sw;
-        __syncthreads();
-        ++phase;
-        int t = 0;
-#pragma unroll
-        for (int w = 0; w < MERGE_THREADS / WAVE; ++w)
-            t += slot[w];
-        return t;
-    };
-    auto count_if = [&](auto pred) -> int {
-        int c = 0;
+    uint64_t prev = 0, pick = ~0ull;
+    for (int r = 0; r < k; ++r) {
+        uint64_t m = ~0ull;
+        auto see = [&](uint64_t v) {
+            if (v > prev && v < m)
+                m = v;
+        };
         if (in_lds) {
-            for (int e = tid; e < total; e += MERGE_THREADS)
-                c += pred(ek[e], ei[e]);
+            for (int e = lane; e < total; e += WAVE)
+                see(ent[e]);
         } else {
 #pragma unroll
-            for (int u = 0; u < LPT; ++u) {
-                const size_t o = base + (size_t)(tid + MERGE_THREADS * u) * k;
+            for (int u = 0; u < LPL; ++u) {
+                const size_t o = base + (size_t)(lane + WAVE * u) * k;
                 for (int j = 0; j < n[u]; ++j)
-                    c += pred(A.ckey[o + j], A.cidx[o + j]);
+                    see(pack(A.ckey[o + j], A.cidx[o + j]));
             }
         }
-        return block_sum(c);
-    };
-    uint32_t prefix = 0;
-    for (int bit = 31; bit >= 0; --bit) {
-        const uint32_t trial = prefix | (1u << bit);
-        if (count_if([&](uint32_t kk, int32_t) { return kk < trial; }) < k)
-            prefix = trial;
+        // wave minimum: the largest complement
+        uint32_t hi = ~(uint32_t)(m >> 32), lo = ~(uint32_t)m;
+        reduce_max_pair<WAVE>(hi, lo);
+        m = ((uint64_t)~hi << 32) | ~lo;
+        if (lane == r)
+            pick = m;
+        prev = m;
     }
-    const uint32_t T = prefix;
-    const int c_lt = count_if([&](uint32_t kk, int32_t) { return kk < T; });
-    const int c_eq = count_if([&](uint32_t kk, int32_t) { return kk == T; });
-    const int r = k - c_lt;
-    int32_t U = IDX_NONE;
-    if (c_eq > r) {
-        uint32_t up = 0;
-        for (int bit = 30; bit >= 0; --bit) {
-            const uint32_t trial = up | (1u << bit);
-            if (count_if([&](uint32_t kk, int32_t ii) { return kk == T && (uint32_t)ii < trial; }) <
-                r)
-                up = trial;
-        }
-        U = (int32_t)up;
-    }
-    // the k selected entries, compacted (their order is fixed below)
-    if (tid < k) {
-        sk[tid] = KEY_NONE;
-        si[tid] = IDX_NONE;
-        so[tid] = IDX_NONE;
-    }
-    __syncthreads();
-    auto take = [&](uint32_t kk, int32_t ii) {
-        if (kk < T || (kk == T && ii <= U)) {
-            const int pos = atomicAdd(&ns_s, 1);
-            if (pos < k) {
-                sk[pos] = kk;
-                si[pos] = ii;
-            }
-        }
-    };
-    if (in_lds) {
-        for (int e = tid; e < total; e += MERGE_THREADS)
-            take(ek[e], ei[e]);
-    } else {
-#pragma unroll
-        for (int u = 0; u < LPT; ++u) {
-            const size_t o = base + (size_t)(tid + MERGE_THREADS * u) * k;
-            for (int j = 0; j < n[u]; ++j)
-                take(A.ckey[o + j], A.cidx[o + j]);
-        }
-    }
-    __syncthreads();
-    if (tid < k) {
-        const uint32_t mk = sk[tid];
-        const int32_t mi = si[tid];
-        int rank = 0;
-        for (int j = 0; j < k; ++j)
-            rank += (sk[j] < mk || (sk[j] == mk && si[j] < mi));
-        A.nbr_idx[(size_t)b * k + rank] = mi;
+    const int32_t pidx = (int32_t)(uint32_t)pick;
+    if (lane < k) {
+        A.nbr_idx[(size_t)b * k + lane] = pidx;
         if (A.nbr_dist)
-            A.nbr_dist[(size_t)b * k + rank] = key2f(mk);
-        so[rank] = mi;
+            A.nbr_dist[(size_t)b * k + lane] = key2f((uint32_t)(pick >> 32));
     }
     if constexpr (PREDICT) {
-        __syncthreads();
-        for (int m = tid; m < A.M; m += MERGE_THREADS)
-            average_labels(so, k, A.qual, A.len, A.N, A.M, m, A.q_hat + (size_t)b * A.M + m,
+        __shared__ int32_t nbr_all[MERGE_WAVES][RB_MAX_K_DEV];
+        int32_t *nbr = nbr_all[wave];
+        if (lane < k)
+            nbr[lane] = pidx;
+        for (int m = lane; m < A.M; m += WAVE)
+            average_labels(nbr, k, A.qual, A.len, A.N, A.M, m, A.q_hat + (size_t)b * A.M + m,
                            A.l_hat + (size_t)b * A.M + m);
     }
 }
@@ -396,13 +340,14 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 thread_local hipEvent_t t_scan_begin = nullptr, t_scan_end = nullptr;
 
-template <int LPT>
+template <int LPL>
 hipError_t launch_merge(const MergeArgs &m, int B, bool predict, hipStream_t s)
 {
+    const dim3 grid((B + MERGE_WAVES - 1) / MERGE_WAVES), block(MERGE_WAVES * WAVE);
     if (predict)
-        hipLaunchKernelGGL((merge_kernel<LPT, true>), dim3(B), dim3(MERGE_THREADS), 0, s, m);
+        hipLaunchKernelGGL((merge_kernel<LPL, true>), grid, block, 0, s, m);
     else
-        hipLaunchKernelGGL((merge_kernel<LPT, false>), dim3(B), dim3(MERGE_THREADS), 0, s, m);
+        hipLaunchKernelGGL((merge_kernel<LPL, false>), grid, block, 0, s, m);
     return hipGetLastError();
 }
 
@@ -625,18 +570,22 @@ hipError_t launch_knn(const KnnPlan &p, const void *queries, const void *bank,
     m.M = M;
     m.q_hat = q_hat;
     m.l_hat = l_hat;
-    const int lpt = (p.W + MERGE_THREADS - 1) / MERGE_THREADS;
+    const int lpl = (p.W + WAVE - 1) / WAVE;
     const bool pred = q_hat != nullptr;
-    if (lpt <= 1)
+    if (lpl <= 1)
         return launch_merge<1>(m, p.B, pred, s);
-    if (lpt <= 2)
+    if (lpl <= 2)
         return launch_merge<2>(m, p.B, pred, s);
-    if (lpt <= 4)
+    if (lpl <= 4)
         return launch_merge<4>(m, p.B, pred, s);
-    if (lpt <= 8)
+    if (lpl <= 8)
         return launch_merge<8>(m, p.B, pred, s);
-    if (lpt <= 16)
+    if (lpl <= 16)
         return launch_merge<16>(m, p.B, pred, s);
+    if (lpl <= 32)
+        return launch_merge<32>(m, p.B, pred, s);
+    if (lpl <= 64)
+        return launch_merge<64>(m, p.B, pred, s);
     return hipErrorInvalidValue;
 }
 

@@ -82,6 +82,8 @@ KNN_CASES = [
     ("bf16", 33, 3000, 2048, 10),   # largest d
     ("f32", 20, 500, 2048, 5),      # largest d, fp32
     ("bf16", 40, 64, 40, 33),       # fewer rows than chunks can use
+    ("bf16", 256, 600, 768, 10),    # no seed sample (N < 64k): every pair of the first
+                                    # iteration is a candidate, most past the LDS staging
 ]
 
 
