@@ -54,7 +54,10 @@ __device__ __forceinline__ T dpp(T x)
 {
     static_assert(sizeof(T) == 4, "32-bit values");
     const int xi = __builtin_bit_cast(int, x);
-    return __builtin_bit_cast(T, __builtin_amdgcn_update_dpp(xi, xi, CTRL, ROW_MASK, 0xf, false));
+    if constexpr (ROW_MASK == 0xf)   // every lane has a source: no old value needed
+        return __builtin_bit_cast(T, __builtin_amdgcn_mov_dpp(xi, CTRL, 0xf, 0xf, true));
+    else
+        return __builtin_bit_cast(T, __builtin_amdgcn_update_dpp(xi, xi, CTRL, ROW_MASK, 0xf, false));
 }
 
 // Butterfly inside each row of 16 lanes (quad permutes, then half-row and row

@@ -109,11 +109,14 @@ __global__ __launch_bounds__(ASSIGN_THREADS) void assign_kernel(
     const int lane = lane_id(), wave = threadIdx.x >> 6;
     const int n_ch = (B + CH - 1) / CH;
     auto inst = [&](int u) { return WIDTH == 16 ? (lane & 15) : lane + WAVE * u; };
+    // maximum over the instance set, as an unsigned maximum of order-preserving
+    // keys (a DPP step folds into one v_max_u32; no NaN canonicalisation)
     auto fmax_all = [&](float v) {
+        const auto umax = [](uint32_t x, uint32_t y) { return x > y ? x : y; };
         if constexpr (WIDTH == 16)
-            return row16_reduce(v, [](float x, float y) { return fmaxf(x, y); });
+            return key2f(row16_reduce(f2key(v), umax));
         else
-            return wave_max(v);
+            return key2f(wave_reduce(f2key(v), umax));
     };
 
     // producers: request r of chunk c into buffer c & 1, one wave per request
