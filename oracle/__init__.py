@@ -9,10 +9,14 @@ The arithmetic lives in ``rb_oracle.c`` (plain C, fp64, scalar loops); this
 module compiles it with gcc on first use and marshals numpy arrays to it.
 Every function follows the passage named in the C source:
   knn      -- exact k nearest neighbours (Sec. 4.2, KNN lookup of Alg. 1)
-  predict  -- uniform KNN mean of per-model quality and length labels (Sec. 4.2)
+  predict  -- KNN mean of per-model quality and length labels, plain or
+              inverse-distance weighted (Sec. 4.2)
   score    -- dense score matrix at the batch-start state (Eq. 1, Eq. 2)
-  score_row-- one request's scores, latencies and costs at a given state
-  assign   -- greedy arrival-order assignment with dead reckoning (Alg. 1, Sec. 4.1-4.2)
+  score_row-- one request's scores, latencies, costs and candidate set at a
+              given state (Eq. 1, Eq. 2, the budget filter of Alg. 1)
+  lpt_order-- longest-predicted-first processing order (Alg. 1, Sec. 4.1)
+  assign   -- greedy assignment with dead reckoning, in arrival or LPT order,
+              over each request's candidate set (Alg. 1, Sec. 4.1-4.2)
   advance  -- drain the state over an inter-batch gap (clamped linear drain)
 """
 from __future__ import annotations
@@ -41,7 +45,7 @@ def build(force: bool = False) -> str:
     if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
         tmp = _LIB + ".tmp%d" % os.getpid()
         subprocess.check_call(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-pthread",
-                               "-Wall", "-Wextra", "-o", tmp, _SRC, "-lm"])
+                               "-ffp-contract=off", "-Wall", "-Wextra", "-o", tmp, _SRC, "-lm"])
         os.replace(tmp, _LIB)
     return _LIB
 
@@ -60,14 +64,21 @@ def _load():
             dbl = ctypes.c_double
             lib.oracle_knn.argtypes = [P, P, i, i, i, i, i, P, P, i]
             lib.oracle_predict.argtypes = [P, i, i, P, P, i, i, P, P]
+            lib.oracle_predict_ex.argtypes = [P, P, i, i, P, P, i, i, i, P, P]
             lib.oracle_score_row.argtypes = [P, P, i, dbl, P, P, P, P, P, P, P, i, dbl, dbl, dbl,
                                              P, P, P]
+            lib.oracle_score_row_ex.argtypes = [P, P, i, dbl, P, P, P, P, P, P, P, i, dbl, dbl,
+                                                dbl, P, P, P, P, P, P]
             lib.oracle_score.argtypes = [P, P, P, i, i, P, P, P, P, P, P, P, i, dbl, dbl, dbl, P]
+            lib.oracle_lpt_order.argtypes = [P, i, i, P]
             lib.oracle_assign.argtypes = [P, P, P, i, i, P, P, P, P, P, P, P, i, dbl, dbl, dbl,
                                           P, P, P, P]
+            lib.oracle_assign_ex.argtypes = [P, P, P, i, i, P, P, P, P, P, P, P, i, dbl, dbl, dbl,
+                                             i, P, P, P, P, P, P, P]
             lib.oracle_advance.argtypes = [P, P, P, P, i, dbl]
-            for f in ("oracle_knn", "oracle_predict", "oracle_score_row", "oracle_score",
-                      "oracle_assign", "oracle_advance"):
+            for f in ("oracle_knn", "oracle_predict", "oracle_predict_ex", "oracle_score_row",
+                      "oracle_score_row_ex", "oracle_score", "oracle_lpt_order", "oracle_assign",
+                      "oracle_assign_ex", "oracle_advance"):
                 getattr(lib, f).restype = ctypes.c_int
             _lib = lib
     return _lib
@@ -124,17 +135,33 @@ def knn(queries, bank, k: int, nthreads: int = 1):
     return idx, dist
 
 
-def predict(nbr, qual, length):
-    """Uniform mean of the neighbours' labels: (q_hat, l_hat), fp64 [B][M]."""
+WEIGHTINGS = {"uniform": 0, "inv_dist": 1}
+ORDERS = ("arrival", "lpt")
+
+
+def predict(nbr, qual, length, dist=None, weighting: str = "uniform"):
+    """KNN-averaged predictions (q_hat, l_hat), fp64 [B][M].
+
+    ``weighting`` "uniform": the plain mean; "inv_dist": weights
+    1/(sqrt(max(dist, 0)) + 1e-6) from the squared distances ``dist`` [B][k],
+    normalised to sum 1.
+    """
     nbr = _c(nbr, np.int32)
     qual = _c(qual, np.float32)
     length = _c(length, np.float32)
     B, k = nbr.shape
     N, M = qual.shape
+    wmode = WEIGHTINGS[weighting]
+    dd = None
+    if wmode:
+        dd = _c(dist, np.float64)
+        if dd.shape != nbr.shape:
+            raise ValueError("dist must have the shape of nbr")
     qh = np.zeros((B, M))
     lh = np.zeros((B, M))
-    _check(_load().oracle_predict(_ptr(nbr), B, k, _ptr(qual), _ptr(length), N, M, _ptr(qh),
-                                  _ptr(lh)), "oracle_predict")
+    _check(_load().oracle_predict_ex(_ptr(nbr), _ptr(dd) if wmode else None, B, k, _ptr(qual),
+                                     _ptr(length), N, M, wmode, _ptr(qh), _ptr(lh)),
+           "oracle_predict_ex")
     return qh, lh
 
 
@@ -144,8 +171,14 @@ def _inst_arrays(inst):
             _c(inst.price_in, np.float64), _c(inst.price_out, np.float64))
 
 
-def score_row(q_hat_r, l_hat_r, plen, inst, p, a, weights):
-    """Scores, latencies and costs of one request at state (p, a): (S, T, C) fp64 [I]."""
+def score_row(q_hat_r, l_hat_r, plen, inst, p, a, weights, budget_r=None, mask=None,
+              with_candidates=False):
+    """Scores, latencies and costs of one request at state (p, a): (S, T, C) fp64 [I].
+
+    ``budget_r`` (a scalar) and ``mask`` [I] restrict the candidate set; the
+    maxima run over the candidates and the others score NaN. With
+    ``with_candidates`` the candidate flags (bool [I]) are returned too.
+    """
     model, _, _, P, D, cin, cout = _inst_arrays(inst)
     q = _c(q_hat_r, np.float64)
     l = _c(l_hat_r, np.float64)
@@ -153,10 +186,16 @@ def score_row(q_hat_r, l_hat_r, plen, inst, p, a, weights):
     a = _c(a, np.float64)
     I = model.shape[0]
     S, T, C = np.zeros(I), np.zeros(I), np.zeros(I)
-    _check(_load().oracle_score_row(_ptr(q), _ptr(l), q.shape[0], float(plen), _ptr(model),
-                                    _ptr(p), _ptr(a), _ptr(P), _ptr(D), _ptr(cin), _ptr(cout), I,
-                                    *map(float, weights), _ptr(S), _ptr(T), _ptr(C)),
-           "oracle_score_row")
+    cand = np.zeros(I, dtype=np.uint8)
+    b = None if budget_r is None else np.array([budget_r], dtype=np.float32)
+    mk = None if mask is None else _c(mask, np.uint8)
+    _check(_load().oracle_score_row_ex(_ptr(q), _ptr(l), q.shape[0], float(plen), _ptr(model),
+                                       _ptr(p), _ptr(a), _ptr(P), _ptr(D), _ptr(cin), _ptr(cout),
+                                       I, *map(float, weights), _ptr(b) if b is not None else None,
+                                       _ptr(mk) if mk is not None else None, _ptr(S), _ptr(T),
+                                       _ptr(C), _ptr(cand)), "oracle_score_row_ex")
+    if with_candidates:
+        return S, T, C, cand.astype(bool)
     return S, T, C
 
 
@@ -175,13 +214,29 @@ def score(q_hat, l_hat, plen, inst, weights):
     return S0
 
 
-def assign(q_hat, l_hat, plen, inst, weights, p=None, a=None, trace=False):
-    """Greedy arrival-order assignment.
+def lpt_order(l_hat):
+    """Longest-predicted-first order of the batch: int32 [B] request indices."""
+    lh = _c(l_hat, np.float64)
+    B, M = lh.shape
+    order = np.zeros(B, dtype=np.int32)
+    _check(_load().oracle_lpt_order(_ptr(lh), B, M, _ptr(order)), "oracle_lpt_order")
+    return order
+
+
+def assign(q_hat, l_hat, plen, inst, weights, p=None, a=None, trace=False, order="arrival",
+           budget=None, mask=None):
+    """Greedy assignment with dead reckoning.
 
     Starts from (p, a) if given (fp64), else from the instances' fp32 state.
-    Returns dict(assign int32 [B], chosen fp64 [B], p, a final fp64 [I]) and,
-    with ``trace``, trace_p / trace_a fp64 [B+1][I] (state before each step).
+    ``order`` is "arrival" or "lpt"; ``budget`` [B] (fp32 per-request cost
+    budgets) and ``mask`` [I] (nonzero = available) restrict each request's
+    candidate set, and a request without candidates gets -1.
+    Returns dict(assign int32 [B], chosen fp64 [B], order int32 [B], p, a final
+    fp64 [I]) and, with ``trace``, trace_p / trace_a fp64 [B+1][I] (state
+    before each step, in processing order).
     """
+    if order not in ORDERS:
+        raise ValueError(f"order must be one of {ORDERS}")
     model, p0, a0, P, D, cin, cout = _inst_arrays(inst)
     p = _c(p0 if p is None else p, np.float64).copy()
     a = _c(a0 if a is None else a, np.float64).copy()
@@ -190,15 +245,25 @@ def assign(q_hat, l_hat, plen, inst, weights, p=None, a=None, trace=False):
     pl = _c(plen, np.int32)
     B, M = qh.shape
     I = model.shape[0]
+    bud = None if budget is None else _c(budget, np.float32)
+    mk = None if mask is None else _c(mask, np.uint8)
+    if bud is not None and bud.shape != (B,):
+        raise ValueError("budget must have shape [B]")
+    if mk is not None and mk.shape != (I,):
+        raise ValueError("mask must have shape [I]")
     out = np.zeros(B, dtype=np.int32)
     chosen = np.zeros(B)
+    ordr = np.zeros(B, dtype=np.int32)
     tp = np.zeros((B + 1, I)) if trace else None
     ta = np.zeros((B + 1, I)) if trace else None
-    _check(_load().oracle_assign(_ptr(qh), _ptr(lh), _ptr(pl), B, M, _ptr(model), _ptr(p), _ptr(a),
-                                 _ptr(P), _ptr(D), _ptr(cin), _ptr(cout), I, *map(float, weights),
-                                 _ptr(out), _ptr(chosen), _ptr(tp) if trace else None,
-                                 _ptr(ta) if trace else None), "oracle_assign")
-    res = {"assign": out, "chosen": chosen, "p": p, "a": a}
+    _check(_load().oracle_assign_ex(_ptr(qh), _ptr(lh), _ptr(pl), B, M, _ptr(model), _ptr(p),
+                                    _ptr(a), _ptr(P), _ptr(D), _ptr(cin), _ptr(cout), I,
+                                    *map(float, weights), int(order == "lpt"),
+                                    _ptr(bud) if bud is not None else None,
+                                    _ptr(mk) if mk is not None else None, _ptr(out),
+                                    _ptr(chosen), _ptr(ordr), _ptr(tp) if trace else None,
+                                    _ptr(ta) if trace else None), "oracle_assign_ex")
+    res = {"assign": out, "chosen": chosen, "order": ordr, "p": p, "a": a}
     if trace:
         res["trace_p"], res["trace_a"] = tp, ta
     return res

@@ -15,20 +15,25 @@ values):
     the oracle's k-th distance (a boundary near-tie); order may differ only
     among near-equal distances; GPU distances of listed rows within 1e-5.
   * predictions: teacher-forced, recomputed by the oracle from the GPU's own
-    neighbour list, within 1e-4.
+    neighbour list (and, for the inverse-distance weights, the GPU's own
+    distances), within 1e-4.
   * scores: from the GPU's predictions, within 1e-4.
   * assignment: teacher-forced replay; each GPU pick must be the oracle's pick
     or score within 1e-5 of the oracle's best (a near tie, counted); the
     replay continues with the GPU's pick; the state after the batch within
     1e-4. Free-running (the oracle on its own): bit-identical picks when the
     replay saw no near tie.
+  * LPT order: the oracle's order from the GPU's predictions, bit-identical
+    to the GPU's (max and comparisons are exact in both precisions).
+  * candidate sets: both sides take the admission test in fp32, so the set
+    must be identical: -1 exactly when it is empty, else a pick inside it.
 """
 from __future__ import annotations
 
 import numpy as np
 
-from . import assign as _assign, knn as _knn, predict as _predict, score as _score, \
-    score_row as _score_row
+from . import assign as _assign, knn as _knn, lpt_order as _lpt_order, predict as _predict, \
+    score as _score, score_row as _score_row
 
 DIST_RTOL = 1e-5
 DIST_FLOOR = 1.0
@@ -86,9 +91,13 @@ def check_neighbours(g_idx, g_dist, o_idx, o_dist, rows=None, label=""):
     return ties
 
 
-def check_predictions(g_idx, g_qhat, g_lhat, qual, length, label=""):
-    """Teacher-forced: the oracle averages the GPU's own neighbour lists."""
-    qh, lh = _predict(np.asarray(g_idx), qual, length)
+def check_predictions(g_idx, g_qhat, g_lhat, qual, length, label="", g_dist=None,
+                      weighting="uniform"):
+    """Teacher-forced: the oracle averages the GPU's own neighbour lists (with
+    the GPU's own distances for the weighted average)."""
+    qh, lh = _predict(np.asarray(g_idx), qual, length,
+                      dist=None if g_dist is None else np.asarray(g_dist, np.float64),
+                      weighting=weighting)
     eq = rel(g_qhat, qh, VAL_FLOOR)
     el = rel(g_lhat, lh, VAL_FLOOR)
     assert eq.max() <= VAL_RTOL, f"{label} q_hat rel err {eq.max()}"
@@ -104,28 +113,47 @@ def check_scores(g_S0, g_qhat, g_lhat, plen, inst, weights, label=""):
 
 
 def check_assign(g_assign, g_chosen, g_qhat, g_lhat, plen, inst, weights, g_final_p=None,
-                 g_final_a=None, p0=None, a0=None, label=""):
-    """Teacher-forced replay of the greedy loop. Returns the near-tie count."""
+                 g_final_a=None, p0=None, a0=None, label="", order="arrival", g_order=None,
+                 budget=None, mask=None):
+    """Teacher-forced replay of the greedy loop. Returns the near-tie count.
+
+    ``order`` "lpt" replays in the oracle's LPT order of the GPU's predictions,
+    which must equal ``g_order`` when given; ``budget`` [B] and ``mask`` [I]
+    restrict the candidate sets as in the GPU call."""
     qh = np.asarray(g_qhat, np.float64)
     lh = np.asarray(g_lhat, np.float64)
     g_assign = np.asarray(g_assign)
+    B = qh.shape[0]
     p = np.asarray(inst.prefill_q if p0 is None else p0, np.float64).copy()
     a = np.asarray(inst.decode_q if a0 is None else a0, np.float64).copy()
     model = np.asarray(inst.model)
+    seq = _lpt_order(lh) if order == "lpt" else np.arange(B)
+    if g_order is not None:
+        assert np.array_equal(np.asarray(g_order), seq), \
+            f"{label} processing order differs at step {int(np.argmax(np.asarray(g_order) != seq))}"
+    budget = None if budget is None else np.asarray(budget, np.float32)
     ties = 0
-    for r in range(qh.shape[0]):
-        S, _, _ = _score_row(qh[r], lh[r], plen[r], inst, p, a, weights)
-        io = int(np.argmax(S))
+    for r in seq:
+        S, _, _, cand = _score_row(qh[r], lh[r], plen[r], inst, p, a, weights,
+                                   budget_r=None if budget is None else budget[r], mask=mask,
+                                   with_candidates=True)
         ig = int(g_assign[r])
-        assert 0 <= ig < S.shape[0], f"{label} step {r}: pick {ig} out of range"
+        if not cand.any():
+            assert ig == -1, f"{label} request {r}: no candidate, gpu picked {ig}"
+            if g_chosen is not None:
+                assert np.isnan(g_chosen[r]), f"{label} request {r}: chosen {g_chosen[r]}"
+            continue
+        assert 0 <= ig < S.shape[0], f"{label} request {r}: pick {ig} out of range"
+        assert cand[ig], f"{label} request {r}: gpu picked {ig}, not a candidate"
+        io = int(np.nanargmax(S))
         if ig != io:
             gap = S[io] - S[ig]
             assert gap <= PICK_RTOL * max(abs(S[io]), SCORE_FLOOR), \
-                f"{label} step {r}: gpu picked {ig} (S={S[ig]}) oracle {io} (S={S[io]})"
+                f"{label} request {r}: gpu picked {ig} (S={S[ig]}) oracle {io} (S={S[io]})"
             ties += 1
         if g_chosen is not None:
             assert rel(g_chosen[r], S[ig], SCORE_FLOOR) <= VAL_RTOL, \
-                f"{label} step {r}: chosen score {g_chosen[r]} vs {S[ig]}"
+                f"{label} request {r}: chosen score {g_chosen[r]} vs {S[ig]}"
         p[ig] += plen[r]
         a[ig] += lh[r, model[ig]]
     if g_final_p is not None:
@@ -137,10 +165,11 @@ def check_assign(g_assign, g_chosen, g_qhat, g_lhat, plen, inst, weights, g_fina
     return ties
 
 
-def free_running(queries, bank, k, qual, length, plen, inst, weights, nthreads=1):
+def free_running(queries, bank, k, qual, length, plen, inst, weights, nthreads=1,
+                 order="arrival", weighting="uniform", budget=None, mask=None):
     """The oracle alone: its own KNN, predictions and greedy loop."""
     idx, dist = _knn(queries, bank, k, nthreads=nthreads)
-    qh, lh = _predict(idx, qual, length)
-    res = _assign(qh, lh, plen, inst, weights)
+    qh, lh = _predict(idx, qual, length, dist=dist, weighting=weighting)
+    res = _assign(qh, lh, plen, inst, weights, order=order, budget=budget, mask=mask)
     res.update(idx=idx, dist=dist, q_hat=qh, l_hat=lh)
     return res

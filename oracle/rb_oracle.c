@@ -16,22 +16,36 @@
  *   - distance: squared Euclidean distance on the stored values (Sec. 4.2
  *     says only "distance-weighted KNN");
  *   - top-k order: distance ascending, ties to the lower bank index;
- *   - averaging: uniform mean over the k neighbours;
+ *   - averaging: uniform mean over the k neighbours by default; the
+ *     distance-weighted option uses w_j = 1/(sqrt(max(d_j, 0)) + 1e-6) on the
+ *     squared distance d_j, normalised to sum 1 (the paper names a
+ *     distance-weighted KNN without giving the weights);
  *   - latency: T = (p_i + l_r)/P_i + (a_i + L_{r,m(i)})/D_i, the instance's
  *     queued prefill plus this prompt drained at its prefill rate, then its
  *     active decode plus this request's predicted output drained at its
  *     decode rate (the state-and-rate form of the estimate in Sec. 4.2);
- *   - normalisation: per request, by the maximum over all instances (Eq. 1);
- *     a zero maximum makes that ratio 0;
+ *   - normalisation: per request, by the maximum over the candidate set
+ *     (Eq. 1; Sec. 4.1 scales by the candidates' maxima); without a budget or
+ *     an availability mask every instance is a candidate; a zero maximum makes
+ *     that ratio 0;
+ *   - candidate set (Alg. 1 budget filter, Eq. 2): an instance is a candidate
+ *     when it is available and its expected cost is at most the request's
+ *     budget; the admission test is taken in fp32, fma(l_r, c_in, L*c_out) <=
+ *     b_r, the precision the GPU path decides it in; a request with no
+ *     candidate is left unassigned (-1) and changes no state;
  *   - argmax ties go to the lowest instance index;
- *   - processing order: arrival order (batch index order);
+ *   - processing order: arrival order (batch index order) by default; the LPT
+ *     option (Alg. 1, Sec. 4.1) sorts by max over models of L[r][m], longest
+ *     first, equal keys in arrival order;
  *   - update after a pick (Sec. 4.2, "Dead reckoning"): p_i* += l_r and
  *     a_i* += L_{r,m(i*)};
  *   - carry between batches: p <- max(0, p - P*dt), a <- max(0, a - D*dt).
  *
  * Parity pins: KNN and predict are pinned by brute force and hand examples;
  * score and assign by a hand-computed 2x3 example and simplex-corner,
- * conservation and scale invariants; carry by its closed form. The paper
+ * conservation and scale invariants; the LPT order, the weighted average and
+ * the candidate set by hand examples, closed forms and a library sort; carry
+ * by its closed form. The paper
  * prints no worked example of its own, so nothing is pinned to a printed
  * paper value.
  */
@@ -147,28 +161,50 @@ int oracle_knn(const void *queries, const void *bank, int dtype, int B, int N, i
 /* quality and output length, one lookup predicts for every model).        */
 /* ------------------------------------------------------------------------ */
 
-/* nbr [B][k] bank indices; qual, len [N][M] fp32. q_hat, l_hat [B][M] are the
- * plain mean over the k neighbours of each model's label. */
-int oracle_predict(const int32_t *nbr, int B, int k, const float *qual, const float *len, int N,
-                   int M, double *q_hat, double *l_hat)
+/* Weight of a neighbour at squared distance d under the distance-weighted
+ * option: the inverse of its Euclidean distance, kept finite at distance 0. */
+static double inv_dist_weight(double d)
+{
+    return 1.0 / (sqrt(fmax(d, 0.0)) + 1e-6);
+}
+
+/* nbr [B][k] bank indices; dist [B][k] their squared distances (read only by
+ * the weighted option); qual, len [N][M] fp32. q_hat, l_hat [B][M] are the
+ * weighted mean over the k neighbours of each model's label, the weights being
+ * 1 (weighting 0, the plain mean) or inv_dist_weight (weighting 1), divided by
+ * their sum. */
+int oracle_predict_ex(const int32_t *nbr, const double *dist, int B, int k, const float *qual,
+                      const float *len, int N, int M, int weighting, double *q_hat,
+                      double *l_hat)
 {
     if (!nbr || !qual || !len || !q_hat || !l_hat || k < 1 || M < 1)
         return -1;
+    if (weighting != 0 && (weighting != 1 || !dist))
+        return -1;
     for (int b = 0; b < B; ++b) {
         for (int m = 0; m < M; ++m) {
-            double sq = 0.0, sl = 0.0;
+            double sq = 0.0, sl = 0.0, sw = 0.0;
             for (int j = 0; j < k; ++j) {
                 int32_t n = nbr[(size_t)b * k + j];
                 if (n < 0 || n >= N)
                     return -1;
-                sq += (double)qual[(size_t)n * M + m];
-                sl += (double)len[(size_t)n * M + m];
+                double wj = weighting ? inv_dist_weight(dist[(size_t)b * k + j]) : 1.0;
+                sq += wj * (double)qual[(size_t)n * M + m];
+                sl += wj * (double)len[(size_t)n * M + m];
+                sw += wj;
             }
-            q_hat[(size_t)b * M + m] = sq / k;
-            l_hat[(size_t)b * M + m] = sl / k;
+            q_hat[(size_t)b * M + m] = sq / sw;
+            l_hat[(size_t)b * M + m] = sl / sw;
         }
     }
     return 0;
+}
+
+/* The plain mean (weighting 0). */
+int oracle_predict(const int32_t *nbr, int B, int k, const float *qual, const float *len, int N,
+                   int M, double *q_hat, double *l_hat)
+{
+    return oracle_predict_ex(nbr, NULL, B, k, qual, len, N, M, 0, q_hat, l_hat);
 }
 
 /* ------------------------------------------------------------------------ */
@@ -181,15 +217,39 @@ typedef struct {
     const double *P, *D, *cin, *cout;
 } orc_inst;
 
+/* Candidate set of one request (Alg. 1 budget filter; Eq. 2): instance i is
+ * a candidate when mask is NULL or mask[i] != 0, and budget_r is NULL or the
+ * expected cost fits it. The cost for this test is computed in fp32 as
+ * fma(l_r, c_in, L*c_out), the precision and rounding the GPU path decides
+ * it in, so both sides admit the same instances. Writes cand[I] (0/1). */
+static void candidates(const double *l_hat_r, double plen, const orc_inst *in, int I,
+                       const float *budget_r, const uint8_t *mask, unsigned char *cand)
+{
+    for (int i = 0; i < I; ++i) {
+        int ok = mask ? mask[i] != 0 : 1;
+        if (ok && budget_r) {
+            float lv = (float)l_hat_r[in->model[i]];
+            float c = fmaf((float)plen, (float)in->cin[i], lv * (float)in->cout[i]);
+            ok = c <= *budget_r;
+        }
+        cand[i] = (unsigned char)ok;
+    }
+}
+
 /* q_hat_r, l_hat_r: this request's [M] predictions; plen: its prompt tokens.
  * p, a: current queued prefill and active decode per instance.
  * w = (w_qual, w_lat, w_cost) in the order of Alg. 1.
- * Writes S[I] and, when non-null, T[I] (latency) and C[I] (cost). */
-static void score_row(const double *q_hat_r, const double *l_hat_r, double plen,
-                      const orc_inst *in, const double *p, const double *a, int I,
-                      const double w[3], double *S, double *T, double *C)
+ * cand [I] (NULL = every instance): the candidate set; the cost and latency
+ * maxima run over it and non-candidates get S = NaN.
+ * Writes S[I], T[I] (latency) and C[I] (cost); returns the number of
+ * candidates. */
+static int score_row(const double *q_hat_r, const double *l_hat_r, double plen,
+                     const orc_inst *in, const double *p, const double *a, int I,
+                     const double w[3], const unsigned char *cand, double *S, double *T,
+                     double *C)
 {
     double tmax = 0.0, cmax = 0.0;
+    int seen = 0;
     for (int i = 0; i < I; ++i) {
         int m = in->model[i];
         /* Eq. 2: input tokens at the input price plus predicted output tokens
@@ -198,35 +258,62 @@ static void score_row(const double *q_hat_r, const double *l_hat_r, double plen,
         /* Latency: queued prefill plus own prompt at the prefill rate, then
          * active decode plus own predicted output at the decode rate. */
         T[i] = (p[i] + plen) / in->P[i] + (a[i] + l_hat_r[m]) / in->D[i];
-        if (i == 0 || C[i] > cmax)
+        if (cand && !cand[i])
+            continue;
+        if (!seen || C[i] > cmax)
             cmax = C[i];
-        if (i == 0 || T[i] > tmax)
+        if (!seen || T[i] > tmax)
             tmax = T[i];
+        seen = 1;
     }
     for (int i = 0; i < I; ++i) {
         int m = in->model[i];
+        if (cand && !cand[i]) {
+            S[i] = NAN;
+            continue;
+        }
         double cost_ratio = cmax > 0.0 ? C[i] / cmax : 0.0;
         double lat_ratio = tmax > 0.0 ? T[i] / tmax : 0.0;
         S[i] = w[0] * q_hat_r[m] + w[2] * (1.0 - cost_ratio) + w[1] * (1.0 - lat_ratio);
     }
+    return seen;
 }
 
-/* One row of scores at a given state, exported for step-by-step replay. */
-int oracle_score_row(const double *q_hat_r, const double *l_hat_r, int M, double plen,
-                     const int32_t *model, const double *p, const double *a, const double *P,
-                     const double *D, const double *cin, const double *cout, int I, double w_qual,
-                     double w_lat, double w_cost, double *S, double *T, double *C)
+/* One row of scores at a given state, exported for step-by-step replay.
+ * budget_r (one value) and mask [I] may be NULL; cand [I] receives the
+ * candidate set (0/1). */
+int oracle_score_row_ex(const double *q_hat_r, const double *l_hat_r, int M, double plen,
+                        const int32_t *model, const double *p, const double *a, const double *P,
+                        const double *D, const double *cin, const double *cout, int I,
+                        double w_qual, double w_lat, double w_cost, const float *budget_r,
+                        const uint8_t *mask, double *S, double *T, double *C,
+                        unsigned char *cand)
 {
     if (!q_hat_r || !l_hat_r || !model || !p || !a || !P || !D || !cin || !cout || !S || !T || !C ||
-        I < 1 || M < 1)
+        !cand || I < 1 || M < 1)
         return -1;
     for (int i = 0; i < I; ++i)
         if (model[i] < 0 || model[i] >= M)
             return -1;
     orc_inst in = {model, P, D, cin, cout};
     double w[3] = {w_qual, w_lat, w_cost};
-    score_row(q_hat_r, l_hat_r, plen, &in, p, a, I, w, S, T, C);
+    candidates(l_hat_r, plen, &in, I, budget_r, mask, cand);
+    score_row(q_hat_r, l_hat_r, plen, &in, p, a, I, w, cand, S, T, C);
     return 0;
+}
+
+int oracle_score_row(const double *q_hat_r, const double *l_hat_r, int M, double plen,
+                     const int32_t *model, const double *p, const double *a, const double *P,
+                     const double *D, const double *cin, const double *cout, int I, double w_qual,
+                     double w_lat, double w_cost, double *S, double *T, double *C)
+{
+    if (I < 1)
+        return -1;
+    unsigned char *cand = (unsigned char *)malloc((size_t)I);
+    int rc = oracle_score_row_ex(q_hat_r, l_hat_r, M, plen, model, p, a, P, D, cin, cout, I,
+                                 w_qual, w_lat, w_cost, NULL, NULL, S, T, C, cand);
+    free(cand);
+    return rc;
 }
 
 /* Dense score matrix S0 [B][I] at the batch-start state. */
@@ -253,17 +340,59 @@ int oracle_score(const double *q_hat, const double *l_hat, const int32_t *plen, 
 /* Greedy online assignment (Alg. 1 loop; Sec. 4.1; dead reckoning, 4.2).   */
 /* ------------------------------------------------------------------------ */
 
-/* For r = 0..B-1 in arrival order: score request r against the current state,
- * pick the highest score (lowest index among equals), record it, then grow the
- * chosen instance's queued prefill by the prompt and its active decode by the
- * request's predicted output on that instance's model.
- * p, a [I] are updated in place. assign [B]; chosen [B] (nullable);
- * trace_p, trace_a [(B+1)][I] (nullable) hold the state before each step and
- * after the last. */
-int oracle_assign(const double *q_hat, const double *l_hat, const int32_t *plen, int B, int M,
-                  const int32_t *model, double *p, double *a, const double *P, const double *D,
-                  const double *cin, const double *cout, int I, double w_qual, double w_lat,
-                  double w_cost, int32_t *assign, double *chosen, double *trace_p, double *trace_a)
+/* LPT processing order (Alg. 1 sorts the batch by predicted length, longest
+ * first; Sec. 4.1 takes the key max over models of L[r][m] because the model
+ * is not chosen yet). Equal keys keep arrival order. */
+typedef struct {
+    double key;
+    int32_t r;
+} lpt_item;
+
+static int lpt_before(const void *x, const void *y)
+{
+    const lpt_item *u = (const lpt_item *)x, *v = (const lpt_item *)y;
+    if (u->key != v->key)
+        return u->key > v->key ? -1 : 1;
+    return u->r < v->r ? -1 : (u->r > v->r);
+}
+
+/* l_hat [B][M]; order [B] receives the request index decided at each step. */
+int oracle_lpt_order(const double *l_hat, int B, int M, int32_t *order)
+{
+    if (!l_hat || !order || B < 0 || M < 1)
+        return -1;
+    lpt_item *it = (lpt_item *)malloc(sizeof(lpt_item) * (size_t)(B > 0 ? B : 1));
+    for (int r = 0; r < B; ++r) {
+        double key = l_hat[(size_t)r * M];
+        for (int m = 1; m < M; ++m)
+            key = fmax(key, l_hat[(size_t)r * M + m]);
+        it[r].key = key;
+        it[r].r = r;
+    }
+    qsort(it, (size_t)B, sizeof(lpt_item), lpt_before);
+    for (int t = 0; t < B; ++t)
+        order[t] = it[t].r;
+    free(it);
+    return 0;
+}
+
+/* For each step t, request r = order[t] (arrival order: r = t; lpt != 0: the
+ * LPT order): form its candidate set, score it against the current state,
+ * pick the highest score among the candidates (lowest index among equals),
+ * record it, then grow the chosen instance's queued prefill by the prompt and
+ * its active decode by the request's predicted output on that instance's
+ * model. A request without candidates gets -1 (chosen NaN) and changes no
+ * state.
+ * p, a [I] are updated in place. budget [B] and mask [I] may be NULL.
+ * assign [B] and chosen [B] (nullable) are indexed by request; order [B]
+ * (nullable) receives the processing order; trace_p, trace_a [(B+1)][I]
+ * (nullable) hold the state before each step and after the last. */
+int oracle_assign_ex(const double *q_hat, const double *l_hat, const int32_t *plen, int B, int M,
+                     const int32_t *model, double *p, double *a, const double *P, const double *D,
+                     const double *cin, const double *cout, int I, double w_qual, double w_lat,
+                     double w_cost, int lpt, const float *budget, const uint8_t *mask,
+                     int32_t *assign, double *chosen, int32_t *order, double *trace_p,
+                     double *trace_a)
 {
     if (!q_hat || !l_hat || !plen || !model || !p || !a || !P || !D || !cin || !cout || !assign ||
         B < 0 || I < 1 || M < 1)
@@ -276,23 +405,36 @@ int oracle_assign(const double *q_hat, const double *l_hat, const int32_t *plen,
     double *S = (double *)malloc(sizeof(double) * (size_t)I);
     double *T = (double *)malloc(sizeof(double) * (size_t)I);
     double *C = (double *)malloc(sizeof(double) * (size_t)I);
-    for (int r = 0; r < B; ++r) {
+    unsigned char *cand = (unsigned char *)malloc((size_t)I);
+    int32_t *ord = (int32_t *)malloc(sizeof(int32_t) * (size_t)(B > 0 ? B : 1));
+    if (lpt)
+        oracle_lpt_order(l_hat, B, M, ord);
+    else
+        for (int t = 0; t < B; ++t)
+            ord[t] = t;
+    for (int t = 0; t < B; ++t) {
+        const int r = ord[t];
         if (trace_p)
-            memcpy(trace_p + (size_t)r * I, p, sizeof(double) * (size_t)I);
+            memcpy(trace_p + (size_t)t * I, p, sizeof(double) * (size_t)I);
         if (trace_a)
-            memcpy(trace_a + (size_t)r * I, a, sizeof(double) * (size_t)I);
+            memcpy(trace_a + (size_t)t * I, a, sizeof(double) * (size_t)I);
         const double *qr = q_hat + (size_t)r * M, *lr = l_hat + (size_t)r * M;
-        score_row(qr, lr, (double)plen[r], &in, p, a, I, w, S, T, C);
-        int best = 0;
-        for (int i = 1; i < I; ++i)
-            if (S[i] > S[best])
+        candidates(lr, (double)plen[r], &in, I, budget ? budget + r : NULL, mask, cand);
+        score_row(qr, lr, (double)plen[r], &in, p, a, I, w, cand, S, T, C);
+        int best = -1;
+        for (int i = 0; i < I; ++i)
+            if (cand[i] && (best < 0 || S[i] > S[best]))
                 best = i;
         assign[r] = best;
         if (chosen)
-            chosen[r] = S[best];
+            chosen[r] = best < 0 ? NAN : S[best];
+        if (best < 0)
+            continue;
         p[best] += (double)plen[r];
         a[best] += lr[model[best]];
     }
+    if (order)
+        memcpy(order, ord, sizeof(int32_t) * (size_t)B);
     if (trace_p)
         memcpy(trace_p + (size_t)B * I, p, sizeof(double) * (size_t)I);
     if (trace_a)
@@ -300,7 +442,19 @@ int oracle_assign(const double *q_hat, const double *l_hat, const int32_t *plen,
     free(S);
     free(T);
     free(C);
+    free(cand);
+    free(ord);
     return 0;
+}
+
+/* Arrival order, every instance a candidate. */
+int oracle_assign(const double *q_hat, const double *l_hat, const int32_t *plen, int B, int M,
+                  const int32_t *model, double *p, double *a, const double *P, const double *D,
+                  const double *cin, const double *cout, int I, double w_qual, double w_lat,
+                  double w_cost, int32_t *assign, double *chosen, double *trace_p, double *trace_a)
+{
+    return oracle_assign_ex(q_hat, l_hat, plen, B, M, model, p, a, P, D, cin, cout, I, w_qual,
+                            w_lat, w_cost, 0, NULL, NULL, assign, chosen, NULL, trace_p, trace_a);
 }
 
 /* ------------------------------------------------------------------------ */

@@ -33,7 +33,7 @@ import torch
 
 __all__ = ["Config", "CONFIGS", "tiny_config", "Instances", "make_centres", "make_embeddings",
            "make_bank", "make_labels", "make_prompt_lens", "make_instances", "make_queries",
-           "simplex_lattice", "Stream"]
+           "make_budgets", "make_availability", "simplex_lattice", "Stream"]
 
 
 @dataclasses.dataclass(frozen=True)
@@ -106,7 +106,8 @@ def tiny_config(**kw) -> Config:
 
 class Stream:
     """Independent child seeds by role: ``Stream(seed).child(role_id)``."""
-    ROLES = {"centres": 0, "bank": 1, "labels": 2, "instances": 3, "queries": 4, "prompts": 5}
+    ROLES = {"centres": 0, "bank": 1, "labels": 2, "instances": 3, "queries": 4, "prompts": 5,
+             "budgets": 6, "availability": 7}
 
     def __init__(self, seed: int):
         self.seq = np.random.SeedSequence(seed)
@@ -249,6 +250,37 @@ def make_instances(cfg: Config) -> Instances:
     f = np.float32
     return Instances(model, p.astype(f), a.astype(f), P.astype(f), D.astype(f),
                      price.astype(f), price.astype(f))
+
+
+def make_budgets(cfg: Config, batch: int = 0, fraction: float = 0.45, lo: float = 0.03,
+                 hi: float = 1.5) -> np.ndarray:
+    """Per-request cost budgets ``[B]`` fp32 (Alg. 1's optional b_r).
+
+    A ``fraction`` of the requests, chosen at random, carry a budget drawn
+    log-uniform in [lo, hi] (the currency of the per-token prices; with the
+    instance prices and the length distributions above, expected request costs
+    run from about 0.04 to 2.2 between their 1st and 99th percentiles); the others carry +inf, i.e. no budget. The paper's
+    budget study constrains 75, 45 or 30 % of the prompts.
+    """
+    rng = Stream(cfg.seed).numpy("budgets", batch + 1)
+    has = rng.uniform(size=cfg.B) < fraction
+    val = np.exp(rng.uniform(math.log(lo), math.log(hi), size=cfg.B))
+    return np.where(has, val, np.inf).astype(np.float32)
+
+
+def make_availability(cfg: Config, lost_models: Sequence[int] = (), down_fraction: float = 0.0
+                      ) -> np.ndarray:
+    """Instance availability ``[I]`` uint8 (1 = available).
+
+    Every instance of a model in ``lost_models`` is unavailable (a lost tier, as
+    in the paper's tier-loss study); of the rest, each is down independently
+    with probability ``down_fraction``.
+    """
+    rng = Stream(cfg.seed).numpy("availability")
+    model = np.concatenate([np.full(c, m, dtype=np.int32) for m, c in enumerate(cfg.inst_per_model)])
+    up = ~np.isin(model, np.asarray(list(lost_models), dtype=np.int32))
+    up &= rng.uniform(size=model.shape[0]) >= down_fraction
+    return up.astype(np.uint8)
 
 
 def simplex_lattice(step: float) -> list:

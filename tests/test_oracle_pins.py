@@ -326,3 +326,213 @@ def test_advance_closed_form():
     assert a1.tolist() == [975.0, 0.0, 0.0]
     with pytest.raises(ValueError):
         oracle.advance(p, a, P, D, -1.0)
+
+
+# ----------------------------------------------------------------------------- LPT order
+
+
+def test_lpt_hand_example():
+    g = _gold("lpt_2x3.json")
+    inst = _inst_from(g)
+    for mode in ("lpt", "arrival"):
+        e = g[mode]
+        r = oracle.assign(g["q_hat"], g["l_hat"], g["prompt_len"], inst, g["weights"], order=mode)
+        assert r["order"].tolist() == e["order"], mode
+        assert r["assign"].tolist() == e["assign"], mode
+        np.testing.assert_allclose(r["chosen"], e["chosen"], rtol=1e-12)
+        np.testing.assert_array_equal(r["p"], e["final_p"])
+        np.testing.assert_array_equal(r["a"], e["final_a"])
+    assert oracle.lpt_order(g["l_hat"]).tolist() == g["lpt"]["order"]
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_lpt_order_matches_library_sort(seed):
+    # independent: numpy's stable lexsort on (descending key, index)
+    rng = np.random.default_rng(100 + seed)
+    B, M = 200, 1 + seed
+    lh = rng.integers(1, 40, (B, M)).astype(np.float64) / 4   # many exactly equal keys
+    key = lh.max(axis=1)
+    expect = np.lexsort((np.arange(B), -key))
+    assert oracle.lpt_order(lh).tolist() == expect.tolist()
+    # a single model: the key is that column
+    assert oracle.lpt_order(lh[:, :1]).tolist() == np.lexsort((np.arange(B), -lh[:, 0])).tolist()
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_lpt_is_arrival_order_over_the_sorted_batch(seed):
+    # LPT decides exactly what the arrival-order loop decides on the batch
+    # permuted into LPT order (Alg. 1 only changes the iteration order)
+    qh, lh, pl, inst = _random_case(200 + seed, B=30)
+    w = (0.3, 0.4, 0.3)
+    r = oracle.assign(qh, lh, pl, inst, w, order="lpt")
+    perm = np.lexsort((np.arange(qh.shape[0]), -lh.max(axis=1)))
+    assert r["order"].tolist() == perm.tolist()
+    ra = oracle.assign(qh[perm], lh[perm], pl[perm], inst, w)
+    assert np.array_equal(r["assign"][perm], ra["assign"])
+    np.testing.assert_array_equal(r["chosen"][perm], ra["chosen"])
+    np.testing.assert_array_equal(r["p"], ra["p"])
+    np.testing.assert_array_equal(r["a"], ra["a"])
+    # equal keys everywhere: LPT is arrival order
+    lh_eq = np.full_like(lh, 123.0)
+    r1 = oracle.assign(qh, lh_eq, pl, inst, w, order="lpt")
+    r2 = oracle.assign(qh, lh_eq, pl, inst, w)
+    assert r1["order"].tolist() == list(range(qh.shape[0]))
+    assert np.array_equal(r1["assign"], r2["assign"])
+
+
+# ----------------------------------------------------------------------------- weighted average
+
+
+def test_inv_dist_weights_closed_forms():
+    qual = np.array([[0.0, 1.0], [1.0, 0.0], [0.25, 0.5]], np.float32)
+    ln = np.array([[10.0, 1.0], [40.0, 2.0], [7.0, 3.0]], np.float32)
+    # squared distances 1 and 4: Euclidean 1 and 2, weights 1/(1+e) and
+    # 1/(2+e) with e = 1e-6, normalised: (2+e)/(3+2e) and (1+e)/(3+2e)
+    e = 1e-6
+    w0, w1 = (2 + e) / (3 + 2 * e), (1 + e) / (3 + 2 * e)
+    qh, lh = oracle.predict([[0, 1]], qual, ln, dist=[[1.0, 4.0]], weighting="inv_dist")
+    np.testing.assert_allclose(qh[0], [w1, w0], rtol=1e-14)
+    np.testing.assert_allclose(lh[0], [10 * w0 + 40 * w1, w0 + 2 * w1], rtol=1e-14)
+    # equal distances: the plain mean, whatever the common distance
+    for dd in (0.0, 0.3, 2.0):
+        qw, lw = oracle.predict([[0, 1, 2]], qual, ln, dist=[[dd] * 3], weighting="inv_dist")
+        qu, lu = oracle.predict([[0, 1, 2]], qual, ln)
+        np.testing.assert_allclose(qw, qu, rtol=1e-14)
+        np.testing.assert_allclose(lw, lu, rtol=1e-14)
+    # k = 1: that row's labels (w*x/w, exact up to one rounding)
+    qh, lh = oracle.predict([[2]], qual, ln, dist=[[0.7]], weighting="inv_dist")
+    np.testing.assert_allclose(qh[0], qual[2].astype(np.float64), rtol=1e-15)
+    np.testing.assert_allclose(lh[0], ln[2].astype(np.float64), rtol=1e-15)
+    # a negative squared distance (cancellation) counts as 0
+    qa, _ = oracle.predict([[0, 1]], qual, ln, dist=[[-0.5, 1.0]], weighting="inv_dist")
+    qb, _ = oracle.predict([[0, 1]], qual, ln, dist=[[0.0, 1.0]], weighting="inv_dist")
+    assert np.array_equal(qa, qb)
+    # the neighbour order does not matter
+    qa, la = oracle.predict([[0, 1, 2]], qual, ln, dist=[[0.1, 0.5, 0.9]], weighting="inv_dist")
+    qb, lb = oracle.predict([[2, 0, 1]], qual, ln, dist=[[0.9, 0.1, 0.5]], weighting="inv_dist")
+    np.testing.assert_allclose(qa, qb, rtol=1e-14)
+    np.testing.assert_allclose(la, lb, rtol=1e-14)
+
+
+def test_inv_dist_hand_example_duplicates_dominate():
+    # the KNN hand example: rows 0 and 4 sit at distance 0 and take weight
+    # 1e6 each against ~1.1 and ~0.7 for the rows at 0.8 and 2, so the
+    # prediction is the mean of rows 0 and 4 to within ~1e-6 relative
+    g = _gold("knn_ties_d2.json")
+    idx, dist = oracle.knn(np.array(g["query"], np.float32), np.array(g["bank"], np.float32),
+                           g["k"])
+    qual = np.array(g["qual"], np.float32)
+    ln = np.array(g["len"], np.float32)
+    qh, lh = oracle.predict(idx, qual, ln, dist=dist, weighting="inv_dist")
+    np.testing.assert_allclose(qh[0], (qual[0] + qual[4]) / 2, rtol=1e-6)
+    np.testing.assert_allclose(lh[0], (ln[0] + ln[4]) / 2, rtol=1e-6)
+    assert not np.allclose(qh[0], g["expect_q_hat"][0], rtol=1e-3)   # differs from the plain mean
+
+
+# ----------------------------------------------------------------------------- candidate sets
+
+
+def _inf(v):
+    return np.float32(np.inf) if v == "inf" else np.float32(v)
+
+
+def test_budget_and_mask_hand_examples():
+    g = _gold("budget_mask_2x3.json")
+    inst = _inst_from(g)
+    for c in g["cases"]:
+        budget = None if c["budget"] is None else np.array([_inf(v) for v in c["budget"]])
+        mask = None if c["mask"] is None else np.array(c["mask"], np.uint8)
+        r = oracle.assign(g["q_hat"], g["l_hat"], g["prompt_len"], inst, g["weights"],
+                          budget=budget, mask=mask)
+        assert r["assign"].tolist() == c["assign"], c["name"]
+        expect = np.array([np.nan if v == "nan" else v for v in c["chosen"]])
+        np.testing.assert_allclose(r["chosen"], expect, rtol=1e-12, equal_nan=True)
+        np.testing.assert_array_equal(r["p"], c["final_p"])
+        np.testing.assert_array_equal(r["a"], c["final_a"])
+    b = g["boundary"]
+    binst = synth.Instances(np.array(b["model"], np.int32), np.zeros(2, np.float32),
+                            np.zeros(2, np.float32), np.array(b["prefill_rate"], np.float32),
+                            np.array(b["decode_rate"], np.float32),
+                            np.array(b["price_in"], np.float32),
+                            np.array(b["price_out"], np.float32))
+    for budget, admitted in b["budgets"]:
+        _, _, C, cand = oracle.score_row(b["q_hat"][0], b["l_hat"][0], b["prompt_len"][0], binst,
+                                         np.zeros(2), np.zeros(2), (0.4, 0.3, 0.3),
+                                         budget_r=budget, with_candidates=True)
+        assert np.flatnonzero(cand).tolist() == admitted, budget
+        np.testing.assert_array_equal(C, [125.0, 300.0])
+        r = oracle.assign(b["q_hat"], b["l_hat"], b["prompt_len"], binst, (0.4, 0.3, 0.3),
+                          budget=np.array([budget], np.float32))
+        assert r["assign"].tolist() == [admitted[0] if admitted else -1]
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_mask_is_removing_instances(seed):
+    # an unavailable instance is as if it were not in the table: the masked
+    # run equals the plain run over the sub-table of available instances
+    qh, lh, pl, inst = _random_case(300 + seed, B=30, I=13)
+    rng = np.random.default_rng(seed)
+    mask = (rng.uniform(size=inst.I) < 0.6).astype(np.uint8)
+    mask[rng.integers(inst.I)] = 1
+    keep = np.flatnonzero(mask)
+    sub = synth.Instances(*(np.asarray(getattr(inst, f))[keep] for f in
+                            ("model", "prefill_q", "decode_q", "prefill_rate", "decode_rate",
+                             "price_in", "price_out")))
+    for order in ("arrival", "lpt"):
+        w = (0.3, 0.4, 0.3)
+        r = oracle.assign(qh, lh, pl, inst, w, mask=mask, order=order)
+        rs = oracle.assign(qh, lh, pl, sub, w, order=order)
+        assert r["assign"].tolist() == keep[rs["assign"]].tolist()
+        np.testing.assert_array_equal(r["chosen"], rs["chosen"])
+        np.testing.assert_array_equal(r["p"][keep], rs["p"])
+        np.testing.assert_array_equal(r["a"][keep], rs["a"])
+        off = np.flatnonzero(mask == 0)
+        np.testing.assert_array_equal(r["p"][off], inst.prefill_q[off])
+        np.testing.assert_array_equal(r["a"][off], inst.decode_q[off])
+    # nothing available: every request unassigned, state unchanged
+    r = oracle.assign(qh, lh, pl, inst, (0.3, 0.4, 0.3), mask=np.zeros(inst.I, np.uint8))
+    assert np.all(r["assign"] == -1) and np.all(np.isnan(r["chosen"]))
+    np.testing.assert_array_equal(r["p"], inst.prefill_q)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_budget_filter_invariants(seed):
+    qh, lh, pl, inst = _random_case(400 + seed, B=30, I=13)
+    w = (0.3, 0.4, 0.3)
+    base = oracle.assign(qh, lh, pl, inst, w, trace=True)
+    # an infinite budget and an all-ones mask change nothing
+    r = oracle.assign(qh, lh, pl, inst, w, budget=np.full(qh.shape[0], np.inf, np.float32),
+                      mask=np.ones(inst.I, np.uint8))
+    assert np.array_equal(r["assign"], base["assign"])
+    np.testing.assert_array_equal(r["chosen"], base["chosen"])
+    # per-request budgets between the cheapest and the dearest instance,
+    # away from every cost (relative gap 1e-3 or more, so precision does not
+    # decide): each pick is an admitted instance and the best among them
+    rng = np.random.default_rng(seed)
+    C = pl[:, None] * inst.price_in[None, :].astype(np.float64) + \
+        lh[:, inst.model] * inst.price_out[None, :].astype(np.float64)
+    budget = np.exp(rng.uniform(np.log(C.min(1)), np.log(C.max(1)))).astype(np.float32)
+    near = np.abs(C / budget[:, None].astype(np.float64) - 1).min(axis=1) < 1e-3
+    budget[near] = np.inf
+    r = oracle.assign(qh, lh, pl, inst, w, budget=budget, trace=True)
+    for t, b in enumerate(r["order"]):
+        admitted = C[b] <= budget[b]
+        i = r["assign"][b]
+        if not admitted.any():
+            assert i == -1
+            continue
+        assert admitted[i]
+        S, _, _ = oracle.score_row(qh[b], lh[b], pl[b], inst, r["trace_p"][t], r["trace_a"][t], w,
+                                   budget_r=budget[b])
+        assert np.all(np.isnan(S[~admitted]))
+        assert i == int(np.nanargmax(S)) and r["chosen"][b] == S[i]
+        # a single admitted instance is its own maximum: S = w_qual * Q
+        if admitted.sum() == 1:
+            assert r["chosen"][b] == w[0] * qh[b][inst.model[i]]
+    # conservation over the admitted picks only
+    got = r["assign"] >= 0
+    for i in range(inst.I):
+        sel = got & (r["assign"] == i)
+        np.testing.assert_allclose(r["p"][i] - inst.prefill_q[i], pl[sel].sum(), rtol=1e-12)
+        np.testing.assert_allclose(r["a"][i] - inst.decode_q[i],
+                                   lh[sel, inst.model[i]].sum(), rtol=1e-12, atol=1e-9)
