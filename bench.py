@@ -10,7 +10,10 @@ already resident in HBM when the timed region starts.
 Default workload: the high-load batch, B=256 requests, N=1,000,000 bank rows,
 d=768 bf16 (1.5 GB), M=4 models, I=13 instances, k=10, weights (1/3,1/3,1/3),
 100 consecutive batches. ``--workload`` selects another of the synthetic
-workloads (tiny, online, highload, largebatch, wide).
+workloads (tiny, online, highload, largebatch, wide). ``--options`` runs the
+path through rb_route_batch_ex with any of: ``lpt`` (longest-predicted-first
+order), ``inv_dist`` (inverse-distance KNN average), ``budget`` (cost budgets
+on 45 % of the requests), ``mask`` (the last model's instances unavailable).
 
 Prints one JSON line with decisions/s (value), the bank-scan bandwidth, the
 roofline of the bank-scan kernel (timed with HIP events on its own stream) and
@@ -75,6 +78,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="highload")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--options", default="",
+                    help="comma list of lpt, inv_dist, budget, mask (rb_route_batch_ex)")
     ap.add_argument("--cpu-sample", type=int, default=0,
                     help="requests in the CPU oracle sample (0: 8 per host thread)")
     ap.add_argument("--record-traffic", metavar="PMC_DIR",
@@ -151,6 +156,10 @@ def main():
     import synth
 
     cfg = synth.CONFIGS[args.workload]
+    opt_names = [o for o in args.options.split(",") if o]
+    bad = set(opt_names) - {"lpt", "inv_dist", "budget", "mask"}
+    if bad:
+        raise SystemExit(f"unknown --options {sorted(bad)}")
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     K, W = args.steps, args.warmup
@@ -173,6 +182,15 @@ def main():
     ws = rb.workspace(cfg.B, cfg.N, cfg.d, dt_code, cfg.k, cfg.M, dev)
     assign = torch.empty(nb, cfg.B, dtype=torch.int32, device=dev)
     carry_dt = cfg.B / 30.0
+    budgets = [torch.from_numpy(synth.make_budgets(cfg, t)).to(dev) if "budget" in opt_names
+               else None for t in range(nb)]
+    mask_h = synth.make_availability(cfg, lost_models=(cfg.M - 1,)) if "mask" in opt_names \
+        else None
+    mask = None if mask_h is None else torch.from_numpy(mask_h).to(dev)
+    opts = [rb.options(order=rb.RB_ORDER_LPT if "lpt" in opt_names else rb.RB_ORDER_ARRIVAL,
+                       weighting=rb.RB_KNN_INV_DIST if "inv_dist" in opt_names
+                       else rb.RB_KNN_UNIFORM, budget=budgets[t], instance_mask=mask)
+            for t in range(nb)] if opt_names else None
     torch.cuda.synchronize()
     log(f"inputs resident in HBM ({time.time() - t0:.1f}s); bank {cfg.bank_bytes() / 1e9:.3f} GB")
 
@@ -183,8 +201,12 @@ def main():
         ev.record(stream)
 
     def step(t):
-        rb.rb_route_batch(queries[t], bank, norms, cfg.k, g_qual, g_len, plens[t], inst,
-                          cfg.weights, ws=ws, assign=assign[t], stream=stream)
+        if opts is None:
+            rb.rb_route_batch(queries[t], bank, norms, cfg.k, g_qual, g_len, plens[t], inst,
+                              cfg.weights, ws=ws, assign=assign[t], stream=stream)
+        else:
+            rb.rb_route_batch_ex(queries[t], bank, norms, cfg.k, g_qual, g_len, plens[t], inst,
+                                 cfg.weights, opts[t], ws=ws, assign=assign[t], stream=stream)
         rb.rb_advance_state(inst, carry_dt, stream=stream)
 
     for t in range(W):
@@ -235,7 +257,8 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(cfg, bank, queries[W], qual, length, plens[W].cpu().numpy(), inst_h,
-                           args.cpu_sample)
+                           args.cpu_sample, opt_names,
+                           None if budgets[W] is None else budgets[W].cpu().numpy(), mask_h)
 
     out = {
         "metric": "routing decisions/sec + bank-scan HBM GB/s (B=256, N=1M, d=768)",
@@ -255,6 +278,7 @@ def main():
                    "B": cfg.B, "N": cfg.N, "d": cfg.d, "k": cfg.k, "M": cfg.M, "I": cfg.I,
                    "weights": [round(w, 6) for w in cfg.weights], "carry_dt_s": round(carry_dt, 6),
                    "parallelism": "single GPU"},
+        "options": opt_names,
         "bank_scan_gbps": round(scan_gbs, 1),
         "arith_intensity_flop_per_byte": round(ai, 1),
         "roofline": roof,
@@ -263,10 +287,12 @@ def main():
     print(json.dumps(out), flush=True)
 
 
-def cpu_baseline(cfg, bank, queries, qual, length, plen, inst_h, sample):
+def cpu_baseline(cfg, bank, queries, qual, length, plen, inst_h, sample, opt_names=(),
+                 budget=None, mask=None):
     """The oracle as it stands on a bounded sample: the first S requests of the
     first timed batch, full k-NN over the whole bank, predictions and the greedy
-    assignment, on all host threads available to this process."""
+    assignment (with the same options), on all host threads available to this
+    process."""
     import numpy as np
 
     import oracle
@@ -276,9 +302,12 @@ def cpu_baseline(cfg, bank, queries, qual, length, plen, inst_h, sample):
     bank_h = bank.cpu()
     q_h = queries[:S].cpu()
     t0 = time.perf_counter()
-    idx, _ = oracle.knn(q_h, bank_h, cfg.k, nthreads=threads)
-    qh, lh = oracle.predict(idx, qual, length)
-    oracle.assign(qh, lh, plen[:S], inst_h, cfg.weights)
+    idx, dist = oracle.knn(q_h, bank_h, cfg.k, nthreads=threads)
+    qh, lh = oracle.predict(idx, qual, length, dist=dist,
+                            weighting="inv_dist" if "inv_dist" in opt_names else "uniform")
+    oracle.assign(qh, lh, plen[:S], inst_h, cfg.weights,
+                  order="lpt" if "lpt" in opt_names else "arrival",
+                  budget=None if budget is None else budget[:S], mask=mask)
     dt = time.perf_counter() - t0
     log(f"cpu baseline: {dt:.1f}s")
     return {"value": round(S / dt, 3), "unit": "decisions/s", "cores": threads, "kind": "oracle",

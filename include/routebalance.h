@@ -54,10 +54,21 @@ typedef enum {
 
 typedef enum { RB_F32 = 0, RB_BF16 = 1 } rb_dtype;
 
-/* Neighbour-averaging rule for rb_predict. Sec. 4.2 calls the paper's KNN
- * "distance-weighted" without giving the weights; this version implements the
- * uniform mean only and returns RB_ERR_UNSUPPORTED for anything else. */
-typedef enum { RB_KNN_UNIFORM = 0 } rb_knn_weighting;
+/* Neighbour-averaging rule (Sec. 4.2 calls the paper's KNN "distance-weighted"
+ * without giving the weights).
+ *   RB_KNN_UNIFORM:   the plain mean over the k neighbours.
+ *   RB_KNN_INV_DIST:  weights w_j = 1/(sqrt(max(d_j, 0)) + 1e-6) on the squared
+ *                     distances d_j (inverse Euclidean distance, finite at 0),
+ *                     normalised to sum 1. */
+typedef enum { RB_KNN_UNIFORM = 0, RB_KNN_INV_DIST = 1 } rb_knn_weighting;
+
+/* Order in which the greedy loop decides the batch.
+ *   RB_ORDER_ARRIVAL: batch index order r = 0..B-1.
+ *   RB_ORDER_LPT:     longest predicted output first (Alg. 1 sorts the batch by
+ *                     predicted length, descending; Sec. 4.1 keys request r by
+ *                     max over m of L[r][m], the model being unknown yet).
+ *                     Equal keys keep arrival order. */
+typedef enum { RB_ORDER_ARRIVAL = 0, RB_ORDER_LPT = 1 } rb_order;
 
 #define RB_MAX_K 64      /* largest neighbour count k */
 #define RB_MAX_D 2048    /* largest embedding dimension d */
@@ -138,12 +149,15 @@ rb_status rb_knn_topk(const void *queries, const void *bank, const float *bank_n
  * candidate model). With RB_KNN_UNIFORM:
  *   q_hat[b][m] = (1/k) * sum_j bank_qual[nbr_idx[b][j]][m]
  *   l_hat[b][m] = (1/k) * sum_j bank_len [nbr_idx[b][j]][m]
- * summed in fp32 in neighbour order j = 0..k-1.
- *   nbr_idx [B][k] int32 in [0, N); nbr_dist [B][k] fp32, unused by the uniform
- *   rule and may be NULL; bank_qual, bank_len [N][M] fp32;
- *   q_hat, l_hat [B][M] fp32 (outputs).
- * Errors: RB_ERR_NULL, RB_ERR_DIMS (B < 0, k < 1, k > RB_MAX_K, N < 1, M < 1,
- * M > RB_MAX_M), RB_ERR_UNSUPPORTED (weighting), RB_ERR_HIP. */
+ * summed in fp32 in neighbour order j = 0..k-1. With RB_KNN_INV_DIST, each
+ * neighbour's labels are weighted by w_j = 1/(sqrt(max(nbr_dist[b][j], 0)) +
+ * 1e-6) and the sums divided by sum_j w_j (fp32, same order).
+ *   nbr_idx [B][k] int32 in [0, N); nbr_dist [B][k] fp32 squared distances as
+ *   rb_knn_topk writes them, unused by the uniform rule and may then be NULL;
+ *   bank_qual, bank_len [N][M] fp32; q_hat, l_hat [B][M] fp32 (outputs).
+ * Errors: RB_ERR_NULL (also nbr_dist NULL with RB_KNN_INV_DIST), RB_ERR_DIMS
+ * (B < 0, k < 1, k > RB_MAX_K, N < 1, M < 1, M > RB_MAX_M), RB_ERR_UNSUPPORTED
+ * (weighting out of range), RB_ERR_HIP. */
 rb_status rb_predict(const int32_t *nbr_idx, const float *nbr_dist, int B, int k,
                      rb_knn_weighting weighting, const float *bank_qual, const float *bank_len,
                      int N, int M, float *q_hat, float *l_hat, void *stream);
@@ -174,6 +188,44 @@ rb_status rb_assign(const float *q_hat, const float *l_hat, const int32_t *promp
                     int M, const rb_instances *inst, int I, rb_weights w, int32_t *assign,
                     float *chosen_score, void *stream);
 
+/* Options of rb_assign_ex and rb_route_batch_ex (a host struct; the pointers
+ * are device pointers). A zero-initialised struct (or a NULL options pointer)
+ * gives the defaults, under which the _ex calls behave as the plain ones.
+ *   order          processing order of the greedy loop (rb_order).
+ *   weighting      neighbour averaging (rb_knn_weighting); read by
+ *                  rb_route_batch_ex only.
+ *   budget         [B] fp32 or NULL: per-request cost budget b_r (Alg. 1 budget
+ *                  filter). Instance i is admitted for request r when its Eq. 2
+ *                  cost fma(l_r, price_in[i], L[r][m(i)]*price_out[i]), in fp32,
+ *                  is <= b_r. +INFINITY means no budget; NaN admits nothing.
+ *   instance_mask  [I] uint8 or NULL: 0 = instance unavailable for this batch
+ *                  (e.g. a lost model tier); NULL = all available.
+ *   order_out      [B] int32 or NULL: receives the processing order,
+ *                  order_out[t] = request decided at step t. Required by
+ *                  rb_assign_ex when order is RB_ORDER_LPT (it also serves as
+ *                  that call's scratch); optional for rb_route_batch_ex.
+ * The candidate set of a request is the available, admitted instances; Eq. 1's
+ * cost and latency maxima run over it (Sec. 4.1: normalised by the candidates'
+ * maxima) and the argmax is taken within it. A request with an empty candidate
+ * set is left unassigned: assign = -1, chosen_score = NaN, no state change. */
+typedef struct {
+    rb_order order;
+    rb_knn_weighting weighting;
+    const float *budget;
+    const uint8_t *instance_mask;
+    int32_t *order_out;
+} rb_options;
+
+/* rb_assign with options (Alg. 1 with its LPT order and budget filter, and an
+ * instance availability mask). assign [B] and chosen_score [B] stay indexed by
+ * request whatever the order. Errors: as rb_assign, plus RB_ERR_UNSUPPORTED
+ * (order or weighting out of range), RB_ERR_NULL (order_out missing for
+ * RB_ORDER_LPT). */
+rb_status rb_assign_ex(const float *q_hat, const float *l_hat, const int32_t *prompt_len, int B,
+                       int M, const rb_instances *inst, int I, rb_weights w,
+                       const rb_options *opts, int32_t *assign, float *chosen_score,
+                       void *stream);
+
 /* The whole path for one batch: rb_knn_topk, then rb_predict (uniform), then
  * rb_assign, enqueued back to back on `stream`. The intermediate outputs
  * nbr_idx [B][k], nbr_dist [B][k], q_hat [B][M], l_hat [B][M] and
@@ -186,6 +238,18 @@ rb_status rb_route_batch(const void *queries, const void *bank, const float *ban
                          const rb_instances *inst, int I, rb_weights w, int32_t *assign,
                          float *chosen_score, int32_t *nbr_idx, float *nbr_dist, float *q_hat,
                          float *l_hat, void *ws, size_t ws_bytes, void *stream);
+
+/* rb_route_batch with options: the averaging rule of opts->weighting, then
+ * rb_assign_ex's order, budgets and mask. The workspace is the same size as
+ * for rb_route_batch (rb_workspace_size). Errors: the union of those of
+ * rb_route_batch and rb_assign_ex (order_out is optional here). */
+rb_status rb_route_batch_ex(const void *queries, const void *bank, const float *bank_norms,
+                            rb_dtype dtype, int B, int N, int d, int k, const float *bank_qual,
+                            const float *bank_len, int M, const int32_t *prompt_len,
+                            const rb_instances *inst, int I, rb_weights w,
+                            const rb_options *opts, int32_t *assign, float *chosen_score,
+                            int32_t *nbr_idx, float *nbr_dist, float *q_hat, float *l_hat,
+                            void *ws, size_t ws_bytes, void *stream);
 
 /* Carry the dead-reckoned state across a gap of dt_seconds between batches:
  *   prefill_q[i] = max(0, prefill_q[i] - prefill_rate[i]*dt)

@@ -23,13 +23,14 @@ LIB_PATH = os.path.join(_HERE, "librouteb.so")
 RB_OK, RB_ERR_NULL, RB_ERR_DIMS, RB_ERR_DTYPE, RB_ERR_WEIGHTS = 0, -1, -2, -3, -4
 RB_ERR_WORKSPACE, RB_ERR_UNSUPPORTED, RB_ERR_HIP, RB_ERR_ALIGN = -5, -6, -7, -8
 RB_F32, RB_BF16 = 0, 1
-RB_KNN_UNIFORM = 0
+RB_KNN_UNIFORM, RB_KNN_INV_DIST = 0, 1
+RB_ORDER_ARRIVAL, RB_ORDER_LPT = 0, 1
 RB_MAX_K, RB_MAX_D, RB_MAX_I, RB_MAX_M = 64, 2048, 1024, 1024
 
 # every symbol include/routebalance.h declares
 EXPORTS = ("rb_status_string", "rb_workspace_size", "rb_bank_norms", "rb_knn_topk", "rb_predict",
-           "rb_score", "rb_assign", "rb_route_batch", "rb_advance_state",
-           "rb_profile_scan_events")
+           "rb_score", "rb_assign", "rb_assign_ex", "rb_route_batch", "rb_route_batch_ex",
+           "rb_advance_state", "rb_profile_scan_events")
 
 
 class RbError(RuntimeError):
@@ -49,6 +50,11 @@ class rb_instances(ctypes.Structure):
                 ("price_out", ctypes.c_void_p)]
 
 
+class rb_options(ctypes.Structure):
+    _fields_ = [("order", ctypes.c_int), ("weighting", ctypes.c_int), ("budget", ctypes.c_void_p),
+                ("instance_mask", ctypes.c_void_p), ("order_out", ctypes.c_void_p)]
+
+
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2606_17949_amd.build`")
@@ -63,8 +69,13 @@ def _load():
         "rb_predict": ([P, P, i, i, i, P, P, i, i, P, P, P], st),
         "rb_score": ([P, P, P, i, i, ctypes.POINTER(rb_instances), i, rb_weights, P, P], st),
         "rb_assign": ([P, P, P, i, i, ctypes.POINTER(rb_instances), i, rb_weights, P, P, P], st),
+        "rb_assign_ex": ([P, P, P, i, i, ctypes.POINTER(rb_instances), i, rb_weights,
+                          ctypes.POINTER(rb_options), P, P, P], st),
         "rb_route_batch": ([P, P, P, i, i, i, i, i, P, P, i, P, ctypes.POINTER(rb_instances), i,
                             rb_weights, P, P, P, P, P, P, P, sz, P], st),
+        "rb_route_batch_ex": ([P, P, P, i, i, i, i, i, P, P, i, P, ctypes.POINTER(rb_instances),
+                               i, rb_weights, ctypes.POINTER(rb_options), P, P, P, P, P, P, P, sz,
+                               P], st),
         "rb_advance_state": ([ctypes.POINTER(rb_instances), i, ctypes.c_float, P], st),
         "rb_profile_scan_events": ([P, P], st),
     }
@@ -273,6 +284,78 @@ def rb_route_batch(queries, bank, bank_norms, k: int, bank_qual, bank_len, promp
                                ctypes.byref(s), inst.I, _w(weights), _ptr(assign), _ptr(chosen),
                                _ptr(nbr_idx), _ptr(nbr_dist), _ptr(q_hat), _ptr(l_hat), _ptr(ws),
                                ws.numel(), _stream(stream)), "rb_route_batch")
+    return assign
+
+
+def options(order: int = RB_ORDER_ARRIVAL, weighting: int = RB_KNN_UNIFORM,
+            budget: Optional[torch.Tensor] = None, instance_mask: Optional[torch.Tensor] = None,
+            order_out: Optional[torch.Tensor] = None) -> rb_options:
+    """An rb_options struct; budget fp32 [B], instance_mask uint8 [I], order_out int32 [B].
+
+    The struct holds references to the tensors, so their memory stays
+    allocated for as long as the struct lives."""
+    for t, dt, name in ((budget, torch.float32, "budget"), (instance_mask, torch.uint8,
+                                                          "instance_mask"),
+                        (order_out, torch.int32, "order_out")):
+        if t is not None and t.dtype != dt:
+            raise ValueError(f"{name}: expected {dt}, got {t.dtype}")
+    o = rb_options(int(order), int(weighting), _ptr(budget), _ptr(instance_mask),
+                   _ptr(order_out))
+    o._tensors = (budget, instance_mask, order_out)
+    return o
+
+
+def _check_opts(opts: rb_options, B: int, I: int):
+    """The option arrays must cover the batch and the instance table."""
+    budget, mask, order_out = getattr(opts, "_tensors", (None, None, None))
+    for t, n, name in ((budget, B, "budget"), (mask, I, "instance_mask"),
+                       (order_out, B, "order_out")):
+        if t is not None and t.numel() != n:
+            raise ValueError(f"{name}: expected {n} elements, got {t.numel()}")
+
+
+def rb_assign_ex(q_hat, l_hat, prompt_len, inst: DeviceInstances, weights, opts: rb_options,
+                 assign: Optional[torch.Tensor] = None, chosen: Optional[torch.Tensor] = None,
+                 stream=None, want_chosen: bool = True):
+    B, M = q_hat.shape
+    dev = q_hat.device
+    if assign is None:
+        assign = torch.empty(B, dtype=torch.int32, device=dev)
+    if chosen is None and want_chosen:
+        chosen = torch.empty(B, dtype=torch.float32, device=dev)
+    _check_opts(opts, B, inst.I)
+    s = inst.struct()
+    _check(_lib.rb_assign_ex(_ptr(q_hat), _ptr(l_hat), _ptr(prompt_len), B, M, ctypes.byref(s),
+                             inst.I, _w(weights), ctypes.byref(opts), _ptr(assign), _ptr(chosen),
+                             _stream(stream)), "rb_assign_ex")
+    return assign, chosen
+
+
+def rb_route_batch_ex(queries, bank, bank_norms, k: int, bank_qual, bank_len, prompt_len,
+                      inst: DeviceInstances, weights, opts: rb_options,
+                      ws: Optional[torch.Tensor] = None, assign: Optional[torch.Tensor] = None,
+                      chosen: Optional[torch.Tensor] = None,
+                      nbr_idx: Optional[torch.Tensor] = None,
+                      nbr_dist: Optional[torch.Tensor] = None,
+                      q_hat: Optional[torch.Tensor] = None, l_hat: Optional[torch.Tensor] = None,
+                      stream=None):
+    """rb_route_batch with options (order, weighting, budgets, availability)."""
+    B, d = queries.shape
+    N = bank.shape[0]
+    M = bank_qual.shape[1]
+    dev = queries.device
+    if assign is None:
+        assign = torch.empty(B, dtype=torch.int32, device=dev)
+    if ws is None:
+        ws = workspace(B, N, d, _dtype_code(bank), k, M, dev)
+    _check_opts(opts, B, inst.I)
+    s = inst.struct()
+    _check(_lib.rb_route_batch_ex(_ptr(queries), _ptr(bank), _ptr(bank_norms), _dtype_code(bank),
+                                  B, N, d, k, _ptr(bank_qual), _ptr(bank_len), M,
+                                  _ptr(prompt_len), ctypes.byref(s), inst.I, _w(weights),
+                                  ctypes.byref(opts), _ptr(assign), _ptr(chosen), _ptr(nbr_idx),
+                                  _ptr(nbr_dist), _ptr(q_hat), _ptr(l_hat), _ptr(ws), ws.numel(),
+                                  _stream(stream)), "rb_route_batch_ex")
     return assign
 
 

@@ -97,10 +97,10 @@ rb::InstArgs inst_args(const rb_instances *in)
     return a;
 }
 
-// Workspace of rb_route_batch beyond the KNN plan: neighbour list and
-// predictions for callers that do not want them back.
+// Workspace of rb_route_batch beyond the KNN plan: neighbour list,
+// predictions and processing order for callers that do not want them back.
 struct RouteExtra {
-    size_t off_nbr, off_qhat, off_lhat, bytes;
+    size_t off_nbr, off_qhat, off_lhat, off_order, bytes;
 };
 
 RouteExtra route_extra(size_t base, int B, int k, int M)
@@ -113,8 +113,41 @@ RouteExtra route_extra(size_t base, int B, int k, int M)
     off += align256((size_t)B * M * 4);
     e.off_lhat = off;
     off += align256((size_t)B * M * 4);
+    e.off_order = off;
+    off += align256((size_t)B * 4);
     e.bytes = off;
     return e;
+}
+
+const rb_options k_default_opts = {RB_ORDER_ARRIVAL, RB_KNN_UNIFORM, nullptr, nullptr, nullptr};
+
+rb_status check_opts(const rb_options *o)
+{
+    if (o->order != RB_ORDER_ARRIVAL && o->order != RB_ORDER_LPT)
+        return RB_ERR_UNSUPPORTED;
+    if (o->weighting != RB_KNN_UNIFORM && o->weighting != RB_KNN_INV_DIST)
+        return RB_ERR_UNSUPPORTED;
+    return RB_OK;
+}
+
+// The greedy loop with options: the LPT order first (into `order`), then the
+// loop over it.
+hipError_t enqueue_assign(const float *qh, const float *lh, const int32_t *plen, int B, int M,
+                          const rb_instances *inst, int I, rb_weights w, const rb_options *o,
+                          int32_t *order, int32_t *assign, float *chosen, hipStream_t st)
+{
+    rb::AssignOpts ao;
+    ao.order = nullptr;
+    ao.budget = o->budget;
+    ao.mask = o->instance_mask;
+    if (o->order == RB_ORDER_LPT) {
+        const hipError_t e = rb::launch_lpt_order(lh, B, M, order, st);
+        if (e != hipSuccess)
+            return e;
+        ao.order = order;
+    }
+    return rb::launch_assign(qh, lh, plen, B, M, inst_args(inst), I, w.w_qual, w.w_lat, w.w_cost,
+                             ao, assign, chosen, st);
 }
 
 rb_status plan(int B, int N, int d, rb_dtype dt, int k, rb::KnnPlan *p)
@@ -128,6 +161,54 @@ rb_status plan(int B, int N, int d, rb_dtype dt, int k, rb::KnnPlan *p)
 }
 
 rb_status hip_status(hipError_t e) { return e == hipSuccess ? RB_OK : RB_ERR_HIP; }
+
+rb_status route_batch(const void *queries, const void *bank, const float *bank_norms,
+                      rb_dtype dtype, int B, int N, int d, int k, const float *bank_qual,
+                      const float *bank_len, int M, const int32_t *prompt_len,
+                      const rb_instances *inst, int I, rb_weights w, const rb_options *o,
+                      int32_t *assign, float *chosen_score, int32_t *nbr_idx, float *nbr_dist,
+                      float *q_hat, float *l_hat, void *ws, size_t ws_bytes, void *stream)
+{
+    rb_status s = check_knn_dims(dtype, B, N, d, k);
+    if (s != RB_OK)
+        return s;
+    if (M < 1 || M > RB_MAX_M)
+        return RB_ERR_DIMS;
+    if ((s = check_inst(inst, I)) != RB_OK)
+        return s;
+    if ((s = check_weights(w)) != RB_OK)
+        return s;
+    if ((s = check_opts(o)) != RB_OK)
+        return s;
+    if (B == 0)
+        return RB_OK;
+    if (!queries || !bank || !bank_norms || !bank_qual || !bank_len || !prompt_len || !assign)
+        return RB_ERR_NULL;
+    if (!aligned(queries, 16) || !aligned(bank, 16))
+        return RB_ERR_ALIGN;
+    rb::KnnPlan p;
+    if ((s = plan(B, N, d, dtype, k, &p)) != RB_OK)
+        return s;
+    const RouteExtra ex = route_extra(p.bytes, B, k, M);
+    if (!ws || ws_bytes < ex.bytes)
+        return RB_ERR_WORKSPACE;
+    if (!aligned(ws, 256))
+        return RB_ERR_ALIGN;
+    uint8_t *wb = (uint8_t *)ws;
+    int32_t *nbr = nbr_idx ? nbr_idx : (int32_t *)(wb + ex.off_nbr);
+    float *qh = q_hat ? q_hat : (float *)(wb + ex.off_qhat);
+    float *lh = l_hat ? l_hat : (float *)(wb + ex.off_lhat);
+    int32_t *order = o->order_out ? o->order_out : (int32_t *)(wb + ex.off_order);
+    hipStream_t st = (hipStream_t)stream;
+    hipError_t e = rb::launch_knn(p, queries, bank, bank_norms, ws, nbr, nbr_dist, bank_qual,
+                                  bank_len, M, qh, lh, o->weighting == RB_KNN_INV_DIST, st);
+    if (e != hipSuccess)
+        return RB_ERR_HIP;
+    e = enqueue_assign(qh, lh, prompt_len, B, M, inst, I, w, o, order, assign, chosen_score, st);
+    if (e == hipSuccess && o->order != RB_ORDER_LPT && o->order_out)
+        e = rb::launch_iota(o->order_out, B, st);
+    return hip_status(e);
+}
 
 }  // namespace
 
@@ -199,24 +280,24 @@ rb_status rb_knn_topk(const void *queries, const void *bank, const float *bank_n
     if (!aligned(ws, 256))
         return RB_ERR_ALIGN;
     return hip_status(rb::launch_knn(p, queries, bank, bank_norms, ws, nbr_idx, nbr_dist, nullptr,
-                                     nullptr, 0, nullptr, nullptr, (hipStream_t)stream));
+                                     nullptr, 0, nullptr, nullptr, false, (hipStream_t)stream));
 }
 
 rb_status rb_predict(const int32_t *nbr_idx, const float *nbr_dist, int B, int k,
                      rb_knn_weighting weighting, const float *bank_qual, const float *bank_len,
                      int N, int M, float *q_hat, float *l_hat, void *stream)
 {
-    (void)nbr_dist;
     if (B < 0 || k < 1 || k > RB_MAX_K || N < 1 || M < 1 || M > RB_MAX_M)
         return RB_ERR_DIMS;
-    if (weighting != RB_KNN_UNIFORM)
+    if (weighting != RB_KNN_UNIFORM && weighting != RB_KNN_INV_DIST)
         return RB_ERR_UNSUPPORTED;
     if (B == 0)
         return RB_OK;
-    if (!nbr_idx || !bank_qual || !bank_len || !q_hat || !l_hat)
+    const bool inv = weighting == RB_KNN_INV_DIST;
+    if (!nbr_idx || !bank_qual || !bank_len || !q_hat || !l_hat || (inv && !nbr_dist))
         return RB_ERR_NULL;
-    return hip_status(rb::launch_predict(nbr_idx, B, k, bank_qual, bank_len, N, M, q_hat, l_hat,
-                                         (hipStream_t)stream));
+    return hip_status(rb::launch_predict(nbr_idx, nbr_dist, B, k, inv, bank_qual, bank_len, N, M,
+                                         q_hat, l_hat, (hipStream_t)stream));
 }
 
 rb_status rb_score(const float *q_hat, const float *l_hat, const int32_t *prompt_len, int B,
@@ -254,9 +335,37 @@ rb_status rb_assign(const float *q_hat, const float *l_hat, const int32_t *promp
         return RB_OK;
     if (!q_hat || !l_hat || !prompt_len || !assign)
         return RB_ERR_NULL;
-    return hip_status(rb::launch_assign(q_hat, l_hat, prompt_len, B, M, inst_args(inst), I,
-                                        w.w_qual, w.w_lat, w.w_cost, assign, chosen_score,
-                                        (hipStream_t)stream));
+    return hip_status(enqueue_assign(q_hat, l_hat, prompt_len, B, M, inst, I, w, &k_default_opts,
+                                     nullptr, assign, chosen_score, (hipStream_t)stream));
+}
+
+rb_status rb_assign_ex(const float *q_hat, const float *l_hat, const int32_t *prompt_len, int B,
+                       int M, const rb_instances *inst, int I, rb_weights w,
+                       const rb_options *opts, int32_t *assign, float *chosen_score,
+                       void *stream)
+{
+    const rb_options *o = opts ? opts : &k_default_opts;
+    if (B < 0 || M < 1 || M > RB_MAX_M)
+        return RB_ERR_DIMS;
+    rb_status s = check_inst(inst, I);
+    if (s != RB_OK)
+        return s;
+    if ((s = check_weights(w)) != RB_OK)
+        return s;
+    if ((s = check_opts(o)) != RB_OK)
+        return s;
+    if (B == 0)
+        return RB_OK;
+    if (!q_hat || !l_hat || !prompt_len || !assign)
+        return RB_ERR_NULL;
+    if (o->order == RB_ORDER_LPT && !o->order_out)
+        return RB_ERR_NULL;
+    hipStream_t st = (hipStream_t)stream;
+    hipError_t e = enqueue_assign(q_hat, l_hat, prompt_len, B, M, inst, I, w, o, o->order_out,
+                                  assign, chosen_score, st);
+    if (e == hipSuccess && o->order != RB_ORDER_LPT && o->order_out)
+        e = rb::launch_iota(o->order_out, B, st);
+    return hip_status(e);
 }
 
 rb_status rb_route_batch(const void *queries, const void *bank, const float *bank_norms,
@@ -266,40 +375,22 @@ rb_status rb_route_batch(const void *queries, const void *bank, const float *ban
                          float *chosen_score, int32_t *nbr_idx, float *nbr_dist, float *q_hat,
                          float *l_hat, void *ws, size_t ws_bytes, void *stream)
 {
-    rb_status s = check_knn_dims(dtype, B, N, d, k);
-    if (s != RB_OK)
-        return s;
-    if (M < 1 || M > RB_MAX_M)
-        return RB_ERR_DIMS;
-    if ((s = check_inst(inst, I)) != RB_OK)
-        return s;
-    if ((s = check_weights(w)) != RB_OK)
-        return s;
-    if (B == 0)
-        return RB_OK;
-    if (!queries || !bank || !bank_norms || !bank_qual || !bank_len || !prompt_len || !assign)
-        return RB_ERR_NULL;
-    if (!aligned(queries, 16) || !aligned(bank, 16))
-        return RB_ERR_ALIGN;
-    rb::KnnPlan p;
-    if ((s = plan(B, N, d, dtype, k, &p)) != RB_OK)
-        return s;
-    const RouteExtra ex = route_extra(p.bytes, B, k, M);
-    if (!ws || ws_bytes < ex.bytes)
-        return RB_ERR_WORKSPACE;
-    if (!aligned(ws, 256))
-        return RB_ERR_ALIGN;
-    uint8_t *wb = (uint8_t *)ws;
-    int32_t *nbr = nbr_idx ? nbr_idx : (int32_t *)(wb + ex.off_nbr);
-    float *qh = q_hat ? q_hat : (float *)(wb + ex.off_qhat);
-    float *lh = l_hat ? l_hat : (float *)(wb + ex.off_lhat);
-    hipStream_t st = (hipStream_t)stream;
-    hipError_t e = rb::launch_knn(p, queries, bank, bank_norms, ws, nbr, nbr_dist, bank_qual,
-                                  bank_len, M, qh, lh, st);
-    if (e != hipSuccess)
-        return RB_ERR_HIP;
-    return hip_status(rb::launch_assign(qh, lh, prompt_len, B, M, inst_args(inst), I, w.w_qual,
-                                        w.w_lat, w.w_cost, assign, chosen_score, st));
+    return route_batch(queries, bank, bank_norms, dtype, B, N, d, k, bank_qual, bank_len, M,
+                       prompt_len, inst, I, w, &k_default_opts, assign, chosen_score, nbr_idx,
+                       nbr_dist, q_hat, l_hat, ws, ws_bytes, stream);
+}
+
+rb_status rb_route_batch_ex(const void *queries, const void *bank, const float *bank_norms,
+                            rb_dtype dtype, int B, int N, int d, int k, const float *bank_qual,
+                            const float *bank_len, int M, const int32_t *prompt_len,
+                            const rb_instances *inst, int I, rb_weights w,
+                            const rb_options *opts, int32_t *assign, float *chosen_score,
+                            int32_t *nbr_idx, float *nbr_dist, float *q_hat, float *l_hat,
+                            void *ws, size_t ws_bytes, void *stream)
+{
+    return route_batch(queries, bank, bank_norms, dtype, B, N, d, k, bank_qual, bank_len, M,
+                       prompt_len, inst, I, w, opts ? opts : &k_default_opts, assign,
+                       chosen_score, nbr_idx, nbr_dist, q_hat, l_hat, ws, ws_bytes, stream);
 }
 
 rb_status rb_profile_scan_events(void *begin, void *end)

@@ -52,13 +52,15 @@ void set_scan_events(hipEvent_t begin, hipEvent_t end);
 
 hipError_t launch_bank_norms(const void *bank, int dtype, int N, int d, float *norms,
                              hipStream_t s);
+// With q_hat non-null, the merge also averages the labels (inv_dist: with
+// inverse-distance weights instead of the plain mean).
 hipError_t launch_knn(const KnnPlan &p, const void *queries, const void *bank,
                       const float *bank_norms, void *ws, int32_t *nbr_idx, float *nbr_dist,
                       const float *bank_qual, const float *bank_len, int M, float *q_hat,
-                      float *l_hat, hipStream_t s);
-hipError_t launch_predict(const int32_t *nbr_idx, int B, int k, const float *bank_qual,
-                          const float *bank_len, int N, int M, float *q_hat, float *l_hat,
-                          hipStream_t s);
+                      float *l_hat, bool inv_dist, hipStream_t s);
+hipError_t launch_predict(const int32_t *nbr_idx, const float *nbr_dist, int B, int k,
+                          bool inv_dist, const float *bank_qual, const float *bank_len, int N,
+                          int M, float *q_hat, float *l_hat, hipStream_t s);
 
 struct InstArgs {
     const int32_t *model;
@@ -69,9 +71,20 @@ struct InstArgs {
 hipError_t launch_score(const float *q_hat, const float *l_hat, const int32_t *plen, int B, int M,
                         const InstArgs &in, int I, float wq, float wl, float wc, float *S0,
                         hipStream_t s);
+// Options of the greedy loop; null pointers are the defaults (arrival order,
+// no budgets, every instance available).
+struct AssignOpts {
+    const int32_t *order;    // [B] request decided at each step
+    const float *budget;     // [B] per-request cost budget
+    const uint8_t *mask;     // [I] nonzero = available
+};
+
+hipError_t launch_lpt_order(const float *l_hat, int B, int M, int32_t *order, hipStream_t s);
+// out[i] = i for i < n (the arrival order, when the caller asks for it).
+hipError_t launch_iota(int32_t *out, int n, hipStream_t s);
 hipError_t launch_assign(const float *q_hat, const float *l_hat, const int32_t *plen, int B,
                          int M, const InstArgs &in, int I, float wq, float wl, float wc,
-                         int32_t *assign, float *chosen, hipStream_t s);
+                         const AssignOpts &opt, int32_t *assign, float *chosen, hipStream_t s);
 hipError_t launch_advance(const InstArgs &in, int I, float dt, hipStream_t s);
 
 }  // namespace rb

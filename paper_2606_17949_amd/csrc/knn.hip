@@ -192,29 +192,54 @@ struct MergeArgs {
     const float *qual, *len;
     int N, M;
     float *q_hat, *l_hat;
+    bool inv_dist;
 };
 
-// The label gather and average: sum over neighbours j = 0..k-1 in order. A
-// neighbour index outside [0, N) makes both averages NaN instead of reading
-// out of bounds (the check does not end the loop, so the k loads can all be
-// in flight together).
-__device__ __forceinline__ void average_labels(const int32_t *nbr, int k, const float *qual,
-                                               const float *len, int N, int M, int m,
-                                               float *q_out, float *l_out)
+// Weight of a neighbour at squared distance d2 in the distance-weighted
+// average: the inverse of its Euclidean distance, finite at distance 0 (a
+// negative d2 from fp32 cancellation counts as 0).
+__device__ __forceinline__ float inv_dist_weight(float d2)
 {
-    float sq = 0.f, sl = 0.f;
+    return 1.f / (sqrtf(fmaxf(d2, 0.f)) + 1e-6f);
+}
+
+// The label gather and average: sum over neighbours j = 0..k-1 in order,
+// divided by k, or (wts non-null) weighted by wts[j] and divided by the sum
+// of the weights. A neighbour index outside [0, N) makes both averages NaN
+// instead of reading out of bounds (the check does not end the loop, so the
+// k loads can all be in flight together).
+__device__ __forceinline__ void average_labels(const int32_t *nbr, const float *wts, int k,
+                                               const float *qual, const float *len, int N, int M,
+                                               int m, float *q_out, float *l_out)
+{
+    float sq = 0.f, sl = 0.f, sw = 0.f;
     bool bad = false;
+    if (wts) {
 #pragma unroll 8
-    for (int j = 0; j < k; ++j) {
-        const int32_t n = nbr[j];
-        const bool ok = n >= 0 && n < N;
-        bad |= !ok;
-        const size_t o = (size_t)(ok ? n : 0) * M + m;
-        sq += qual[o];
-        sl += len[o];
+        for (int j = 0; j < k; ++j) {
+            const int32_t n = nbr[j];
+            const bool ok = n >= 0 && n < N;
+            bad |= !ok;
+            const size_t o = (size_t)(ok ? n : 0) * M + m;
+            const float w = wts[j];
+            sq = fmaf(w, qual[o], sq);
+            sl = fmaf(w, len[o], sl);
+            sw += w;
+        }
+    } else {
+#pragma unroll 8
+        for (int j = 0; j < k; ++j) {
+            const int32_t n = nbr[j];
+            const bool ok = n >= 0 && n < N;
+            bad |= !ok;
+            const size_t o = (size_t)(ok ? n : 0) * M + m;
+            sq += qual[o];
+            sl += len[o];
+        }
+        sw = (float)k;
     }
-    *q_out = bad ? __builtin_nanf("") : sq / (float)k;
-    *l_out = bad ? __builtin_nanf("") : sl / (float)k;
+    *q_out = bad ? __builtin_nanf("") : sq / sw;
+    *l_out = bad ? __builtin_nanf("") : sl / sw;
 }
 
 // One wave per query (MERGE_WAVES queries per workgroup, no workgroup
@@ -309,29 +334,39 @@ __global__ __launch_bounds__(MERGE_WAVES * WAVE) void merge_kernel(const MergeAr
     }
     if constexpr (PREDICT) {
         __shared__ int32_t nbr_all[MERGE_WAVES][RB_MAX_K_DEV];
+        __shared__ float wts_all[MERGE_WAVES][RB_MAX_K_DEV];
         int32_t *nbr = nbr_all[wave];
-        if (lane < k)
+        float *wts = wts_all[wave];
+        if (lane < k) {
             nbr[lane] = pidx;
+            wts[lane] = inv_dist_weight(key2f((uint32_t)(pick >> 32)));
+        }
         for (int m = lane; m < A.M; m += WAVE)
-            average_labels(nbr, k, A.qual, A.len, A.N, A.M, m, A.q_hat + (size_t)b * A.M + m,
-                           A.l_hat + (size_t)b * A.M + m);
+            average_labels(nbr, A.inv_dist ? wts : nullptr, k, A.qual, A.len, A.N, A.M, m,
+                           A.q_hat + (size_t)b * A.M + m, A.l_hat + (size_t)b * A.M + m);
     }
 }
 
-__global__ __launch_bounds__(64) void predict_kernel(const int32_t *__restrict__ nbr_idx, int k,
+// One workgroup per request; nbr_dist is read only for the weighted average.
+__global__ __launch_bounds__(64) void predict_kernel(const int32_t *__restrict__ nbr_idx,
+                                                     const float *__restrict__ nbr_dist, int k,
                                                      const float *__restrict__ qual,
                                                      const float *__restrict__ len, int N, int M,
                                                      float *__restrict__ q_hat,
                                                      float *__restrict__ l_hat)
 {
     __shared__ int32_t nbr[RB_MAX_K_DEV];
+    __shared__ float wts[RB_MAX_K_DEV];
     const int b = blockIdx.x;
-    for (int j = threadIdx.x; j < k; j += blockDim.x)
+    for (int j = threadIdx.x; j < k; j += blockDim.x) {
         nbr[j] = nbr_idx[(size_t)b * k + j];
+        if (nbr_dist)
+            wts[j] = inv_dist_weight(nbr_dist[(size_t)b * k + j]);
+    }
     __syncthreads();
     for (int m = threadIdx.x; m < M; m += blockDim.x)
-        average_labels(nbr, k, qual, len, N, M, m, q_hat + (size_t)b * M + m,
-                       l_hat + (size_t)b * M + m);
+        average_labels(nbr, nbr_dist ? wts : nullptr, k, qual, len, N, M, m,
+                       q_hat + (size_t)b * M + m, l_hat + (size_t)b * M + m);
 }
 
 // ------------------------------------------------------------------ host side
@@ -487,7 +522,7 @@ hipError_t launch_bank_norms(const void *bank, int dtype, int N, int d, float *n
 hipError_t launch_knn(const KnnPlan &p, const void *queries, const void *bank,
                       const float *bank_norms, void *ws, int32_t *nbr_idx, float *nbr_dist,
                       const float *bank_qual, const float *bank_len, int M, float *q_hat,
-                      float *l_hat, hipStream_t s)
+                      float *l_hat, bool inv_dist, hipStream_t s)
 {
     uint8_t *w = (uint8_t *)ws;
     uint32_t *tau = (uint32_t *)(w + p.off_tau);
@@ -570,6 +605,7 @@ hipError_t launch_knn(const KnnPlan &p, const void *queries, const void *bank,
     m.M = M;
     m.q_hat = q_hat;
     m.l_hat = l_hat;
+    m.inv_dist = inv_dist;
     const int lpl = (p.W + WAVE - 1) / WAVE;
     const bool pred = q_hat != nullptr;
     if (lpl <= 1)
@@ -589,12 +625,12 @@ hipError_t launch_knn(const KnnPlan &p, const void *queries, const void *bank,
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_predict(const int32_t *nbr_idx, int B, int k, const float *bank_qual,
-                          const float *bank_len, int N, int M, float *q_hat, float *l_hat,
-                          hipStream_t s)
+hipError_t launch_predict(const int32_t *nbr_idx, const float *nbr_dist, int B, int k,
+                          bool inv_dist, const float *bank_qual, const float *bank_len, int N,
+                          int M, float *q_hat, float *l_hat, hipStream_t s)
 {
-    hipLaunchKernelGGL(predict_kernel, dim3(B), dim3(64), 0, s, nbr_idx, k, bank_qual, bank_len,
-                       N, M, q_hat, l_hat);
+    hipLaunchKernelGGL(predict_kernel, dim3(B), dim3(64), 0, s, nbr_idx,
+                       inv_dist ? nbr_dist : nullptr, k, bank_qual, bank_len, N, M, q_hat, l_hat);
     return hipGetLastError();
 }
 

@@ -80,16 +80,59 @@ __global__ __launch_bounds__(256) void score_kernel(const float *__restrict__ q_
     }
 }
 
+// Longest-predicted-first order (Alg. 1; Sec. 4.1 keys a request by the
+// maximum over models of its predicted length). Each request's position is
+// the number of requests before it under (key descending, index ascending),
+// a total order, so the positions form a permutation: order[pos] = r. Every
+// workgroup ranks LPT_THREADS requests against all B keys, which it computes
+// tile by tile into LDS.
+constexpr int LPT_THREADS = 256;
+
+__global__ __launch_bounds__(LPT_THREADS) void lpt_order_kernel(const float *__restrict__ l_hat,
+                                                                 int B, int M,
+                                                                 int32_t *__restrict__ order)
+{
+    __shared__ uint64_t keys[LPT_THREADS];
+    // ascending in this 64-bit key is descending in the length, then
+    // ascending in the index
+    auto key_of = [&](int r) {
+        const float *row = l_hat + (size_t)r * M;
+        float mx = row[0];
+        for (int m = 1; m < M; ++m)
+            mx = fmaxf(mx, row[m]);
+        return ((uint64_t)~f2key(mx) << 32) | (uint32_t)r;
+    };
+    const int r = blockIdx.x * LPT_THREADS + threadIdx.x;
+    const uint64_t mine = r < B ? key_of(r) : ~0ull;
+    int pos = 0;
+    for (int base = 0; base < B; base += LPT_THREADS) {
+        const int s = base + threadIdx.x;
+        keys[threadIdx.x] = s < B ? key_of(s) : ~0ull;
+        __syncthreads();
+        const int n = min(LPT_THREADS, B - base);
+        for (int j = 0; j < n; ++j)
+            pos += keys[j] < mine ? 1 : 0;
+        __syncthreads();
+    }
+    if (r < B)
+        order[pos] = r;
+}
+
 // Greedy assignment. Wave 0 runs the sequential loop over requests; waves
-// 1..15 fill, one chunk of requests ahead, an LDS double buffer with what does
+// 1..15 fill, one chunk of steps ahead, an LDS double buffer with what does
 // not depend on the state: per (request, instance) the base score and the
-// predicted output length on the instance's model. WIDTH = 16 (I <= 16):
+// predicted output length on the instance's model. Step t decides request
+// order[t] (arrival order when order is null). An instance outside the
+// request's candidate set (unavailable in mask, or over the request's budget
+// in the Eq. 2 cost) gets a NaN base score: it is left out of both maxima and
+// never picked. WIDTH = 16 (I <= 16):
 // instance i = lane % 16, replicated in the four rows of 16 lanes, so every
 // reduction stays inside a row and leaves its result in every lane. WIDTH = 64:
 // instance i = lane + 64*u in register slot u. Per request: the latency
 // maximum (one reduction), the scores, then one reduction of (score key,
 // ~instance) pairs that yields the largest score and, among equal scores, the
 // lowest instance index; the lanes holding that instance update its state.
+// A request without candidates gets -1 and changes no state.
 constexpr int ASSIGN_THREADS = 1024;
 constexpr int ASSIGN_WAVES = ASSIGN_THREADS / WAVE;
 constexpr int ASSIGN_LDS_FLOATS = 8192;   // per buffer: chunk rows x instances x 2
@@ -98,7 +141,7 @@ template <int IPL, int WIDTH>
 __global__ __launch_bounds__(ASSIGN_THREADS) void assign_kernel(
     const float *__restrict__ q_hat, const float *__restrict__ l_hat,
     const int32_t *__restrict__ plen, int B, int M, const InstArgs in, int I, float wq, float wl,
-    float wc, int32_t *__restrict__ assign, float *__restrict__ chosen)
+    float wc, const AssignOpts opt, int32_t *__restrict__ assign, float *__restrict__ chosen)
 {
     static_assert(WIDTH == 64 || IPL == 1, "a 16-lane row holds one slot");
     constexpr int IP = IPL * WIDTH;                       // instances per LDS row
@@ -106,6 +149,7 @@ __global__ __launch_bounds__(ASSIGN_THREADS) void assign_kernel(
     __shared__ float base_s[2][CH][IP];
     __shared__ float lv_s[2][CH][IP];
     __shared__ float l_s[2][CH];
+    __shared__ int32_t r_s[2][CH];
     const int lane = lane_id(), wave = threadIdx.x >> 6;
     const int n_ch = (B + CH - 1) / CH;
     auto inst = [&](int u) { return WIDTH == 16 ? (lane & 15) : lane + WAVE * u; };
@@ -119,17 +163,20 @@ __global__ __launch_bounds__(ASSIGN_THREADS) void assign_kernel(
             return key2f(wave_reduce(f2key(v), umax));
     };
 
-    // producers: request r of chunk c into buffer c & 1, one wave per request
+    // producers: step t = c*CH + j into slot j of buffer c & 1, one wave per step
     auto produce = [&](int c) {
         const int buf = c & 1;
         for (int j = wave - 1; j < CH; j += ASSIGN_WAVES - 1) {
-            const int r = c * CH + j;
-            if (r >= B)
+            const int t = c * CH + j;
+            if (t >= B)
                 break;
+            const int r = opt.order ? opt.order[t] : t;
             const float l = (float)plen[r];
             const float *qr = q_hat + (size_t)r * M;
             const float *lr = l_hat + (size_t)r * M;
+            const float budget = opt.budget ? opt.budget[r] : INFINITY;
             float qv[IPL], lv[IPL], C[IPL];
+            bool cand[IPL];
             float cmax = -INFINITY;
 #pragma unroll
             for (int u = 0; u < IPL; ++u) {
@@ -139,19 +186,24 @@ __global__ __launch_bounds__(ASSIGN_THREADS) void assign_kernel(
                 qv[u] = ok ? qr[m] : 0.f;
                 lv[u] = ok ? lr[m] : 0.f;
                 C[u] = cost(l, lv[u], ok ? in.cin[i] : 0.f, ok ? in.cout[i] : 0.f);
-                if (ok)
+                // Alg. 1 budget filter on the Eq. 2 cost, and availability
+                cand[u] = ok && (!opt.mask || opt.mask[i] != 0) && C[u] <= budget;
+                if (cand[u])
                     cmax = fmaxf(cmax, C[u]);
             }
             cmax = fmax_all(cmax);
             if (lane < (WIDTH == 16 ? 16 : WAVE)) {
 #pragma unroll
                 for (int u = 0; u < IPL; ++u) {
-                    base_s[buf][j][lane + WAVE * u] = base_score(qv[u], C[u], cmax, wq, wc);
+                    base_s[buf][j][lane + WAVE * u] =
+                        cand[u] ? base_score(qv[u], C[u], cmax, wq, wc) : __builtin_nanf("");
                     lv_s[buf][j][lane + WAVE * u] = lv[u];
                 }
             }
-            if (lane == 0)
+            if (lane == 0) {
                 l_s[buf][j] = l;
+                r_s[buf][j] = r;
+            }
         }
     };
 
@@ -186,16 +238,17 @@ __global__ __launch_bounds__(ASSIGN_THREADS) void assign_kernel(
         const int buf = c & 1;
         const int rows = min(CH, B - c * CH);
         float l = l_s[buf][0], bs[IPL], lv[IPL];
+        int r = r_s[buf][0];
 #pragma unroll
         for (int u = 0; u < IPL; ++u) {
             bs[u] = base_s[buf][0][col + WAVE * u];
             lv[u] = lv_s[buf][0][col + WAVE * u];
         }
         for (int j = 0; j < rows; ++j) {
-            const int r = c * CH + j;
-            // next request's values, in flight while this one is decided
+            // next step's values, in flight while this one is decided
             const int jn = j + 1 < rows ? j + 1 : j;
             const float ln = l_s[buf][jn];
+            const int rn = r_s[buf][jn];
             float bsn[IPL], lvn[IPL];
 #pragma unroll
             for (int u = 0; u < IPL; ++u) {
@@ -207,7 +260,7 @@ __global__ __launch_bounds__(ASSIGN_THREADS) void assign_kernel(
 #pragma unroll
             for (int u = 0; u < IPL; ++u) {
                 T[u] = latency(p[u], a[u], rP[u], rD[u], l, lv[u]);
-                if (valid[u])
+                if (bs[u] == bs[u])   // a candidate
                     tmax = fmaxf(tmax, T[u]);
             }
             tmax = fmax_all(tmax);
@@ -217,7 +270,7 @@ __global__ __launch_bounds__(ASSIGN_THREADS) void assign_kernel(
             for (int u = 0; u < IPL; ++u) {
                 const float S = full_score(bs[u], T[u], tmax, wl);
                 const uint32_t key = f2key(S);
-                if (valid[u] && S == S && key > best) {   // slots ascend in index: ties keep the lower
+                if (S == S && key > best) {   // slots ascend in index: ties keep the lower
                     best = key;
                     bu = u;
                 }
@@ -225,7 +278,7 @@ __global__ __launch_bounds__(ASSIGN_THREADS) void assign_kernel(
             uint32_t hi = best, lo = best ? ~(uint32_t)inst(bu) : 0u;
             reduce_max_pair<WIDTH>(hi, lo);
             const bool found = hi != 0;
-            const int istar = found ? (int)~lo : 0;
+            const int istar = found ? (int)~lo : -1;
             if (lane == 0) {
                 assign[r] = istar;
                 if (chosen)
@@ -239,6 +292,7 @@ __global__ __launch_bounds__(ASSIGN_THREADS) void assign_kernel(
                 }
             }
             l = ln;
+            r = rn;
 #pragma unroll
             for (int u = 0; u < IPL; ++u) {
                 bs[u] = bsn[u];
@@ -255,6 +309,13 @@ __global__ __launch_bounds__(ASSIGN_THREADS) void assign_kernel(
             in.a[i] = a[u];
         }
     }
+}
+
+__global__ __launch_bounds__(256) void iota_kernel(int32_t *__restrict__ out, int n)
+{
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n)
+        out[i] = i;
 }
 
 __global__ __launch_bounds__(256) void advance_kernel(const InstArgs in, int I, float dt)
@@ -277,14 +338,21 @@ hipError_t launch_score(const float *q_hat, const float *l_hat, const int32_t *p
     return hipGetLastError();
 }
 
+hipError_t launch_lpt_order(const float *l_hat, int B, int M, int32_t *order, hipStream_t s)
+{
+    hipLaunchKernelGGL(lpt_order_kernel, dim3((B + LPT_THREADS - 1) / LPT_THREADS),
+                       dim3(LPT_THREADS), 0, s, l_hat, B, M, order);
+    return hipGetLastError();
+}
+
 hipError_t launch_assign(const float *q_hat, const float *l_hat, const int32_t *plen, int B,
                          int M, const InstArgs &in, int I, float wq, float wl, float wc,
-                         int32_t *assign, float *chosen, hipStream_t s)
+                         const AssignOpts &opt, int32_t *assign, float *chosen, hipStream_t s)
 {
     const int ipl = (I + WAVE - 1) / WAVE;
 #define RB_ASSIGN(N, W)                                                                          \
     hipLaunchKernelGGL((assign_kernel<N, W>), dim3(1), dim3(ASSIGN_THREADS), 0, s, q_hat, l_hat, \
-                       plen, B, M, in, I, wq, wl, wc, assign, chosen)
+                       plen, B, M, in, I, wq, wl, wc, opt, assign, chosen)
     if (I <= 16) RB_ASSIGN(1, 16);
     else if (ipl <= 1) RB_ASSIGN(1, 64);
     else if (ipl <= 2) RB_ASSIGN(2, 64);
@@ -293,6 +361,12 @@ hipError_t launch_assign(const float *q_hat, const float *l_hat, const int32_t *
     else if (ipl <= 16) RB_ASSIGN(16, 64);
     else return hipErrorInvalidValue;
 #undef RB_ASSIGN
+    return hipGetLastError();
+}
+
+hipError_t launch_iota(int32_t *out, int n, hipStream_t s)
+{
+    hipLaunchKernelGGL(iota_kernel, dim3((n + 255) / 256), dim3(256), 0, s, out, n);
     return hipGetLastError();
 }
 

@@ -93,7 +93,8 @@ def test_predict_validation():
     args = lambda **kw: (kw.get("nbr", FAKE), None, kw.get("B", 4), kw.get("k", 10),
                          kw.get("wt", rb.RB_KNN_UNIFORM), kw.get("qual", FAKE), FAKE,
                          kw.get("N", 100), kw.get("M", 4), FAKE, FAKE, None)
-    assert L.rb_predict(*args(wt=1)) == rb.RB_ERR_UNSUPPORTED
+    assert L.rb_predict(*args(wt=2)) == rb.RB_ERR_UNSUPPORTED
+    assert L.rb_predict(*args(wt=rb.RB_KNN_INV_DIST)) == rb.RB_ERR_NULL   # needs nbr_dist
     assert L.rb_predict(*args(k=0)) == rb.RB_ERR_DIMS
     assert L.rb_predict(*args(k=65)) == rb.RB_ERR_DIMS
     assert L.rb_predict(*args(M=0)) == rb.RB_ERR_DIMS
@@ -165,6 +166,71 @@ def test_route_batch_validation():
     assert call(inst=None) == rb.RB_ERR_NULL
     assert call(q=MISALIGNED) == rb.RB_ERR_ALIGN
     assert call(B=0, q=None, asg=None, pl=None) == rb.RB_OK
+
+
+def test_assign_ex_validation():
+    s = _inst()
+
+    def call(opts=None, **kw):
+        a = dict(q=FAKE, B=4, M=4, inst=ctypes.byref(s), I=13, w=W, asg=FAKE)
+        a.update(kw)
+        o = None if opts is None else ctypes.byref(opts)
+        return L.rb_assign_ex(a["q"], FAKE, FAKE, a["B"], a["M"], a["inst"], a["I"], a["w"], o,
+                              a["asg"], None, None)
+    assert call(rb.rb_options(2, 0, None, None, None)) == rb.RB_ERR_UNSUPPORTED
+    assert call(rb.rb_options(0, 5, None, None, None)) == rb.RB_ERR_UNSUPPORTED
+    assert call(rb.rb_options(-1, 0, None, None, None)) == rb.RB_ERR_UNSUPPORTED
+    # LPT needs order_out
+    assert call(rb.rb_options(rb.RB_ORDER_LPT, 0, None, None, None)) == rb.RB_ERR_NULL
+    assert call(rb.rb_options(0, 0, None, None, None), asg=None) == rb.RB_ERR_NULL
+    assert call(None, M=0) == rb.RB_ERR_DIMS
+    assert call(None, I=1025) == rb.RB_ERR_DIMS
+    assert call(None, w=rb.rb_weights(1, 1, 0)) == rb.RB_ERR_WEIGHTS
+    assert call(rb.rb_options(rb.RB_ORDER_LPT, 0, None, None, None), B=0, q=None,
+                asg=None) == rb.RB_OK
+
+
+def test_route_batch_ex_validation():
+    s = _inst()
+
+    def call(opts, **kw):
+        a = dict(q=FAKE, B=4, asg=FAKE)
+        a.update(kw)
+        return L.rb_route_batch_ex(a["q"], FAKE, FAKE, rb.RB_BF16, a["B"], 100, 64, 10, FAKE, FAKE,
+                                   4, FAKE, ctypes.byref(s), 13, W,
+                                   None if opts is None else ctypes.byref(opts), a["asg"], None,
+                                   None, None, None, None, FAKE, 1 << 20, None)
+    assert call(rb.rb_options(3, 0, None, None, None)) == rb.RB_ERR_UNSUPPORTED
+    assert call(rb.rb_options(0, 3, None, None, None)) == rb.RB_ERR_UNSUPPORTED
+    assert call(None, asg=None) == rb.RB_ERR_NULL
+    assert call(None, q=MISALIGNED) == rb.RB_ERR_ALIGN
+    assert call(rb.rb_options(rb.RB_ORDER_LPT, rb.RB_KNN_INV_DIST, None, None, None), B=0, q=None,
+                asg=None) == rb.RB_OK
+
+
+def test_struct_layouts_match_the_header(tmp_path):
+    # the C compiler's layout of the header's structs against the binding's
+    src = tmp_path / "layout.c"
+    src.write_text(
+        '#include <stdio.h>\n#include <stddef.h>\n#include "routebalance.h"\n'
+        'int main(void) {\n'
+        '  printf("%zu %zu %zu %zu %zu %zu\\n", sizeof(rb_options), offsetof(rb_options, weighting),\n'
+        '         offsetof(rb_options, budget), offsetof(rb_options, instance_mask),\n'
+        '         offsetof(rb_options, order_out), sizeof(rb_instances));\n'
+        '  printf("%zu %zu\\n", sizeof(rb_weights), offsetof(rb_weights, w_cost));\n'
+        '  return 0;\n}\n')
+    exe = tmp_path / "layout"
+    subprocess.check_call(["gcc", "-std=c11", "-I", os.path.dirname(HEADER), "-o", str(exe),
+                           str(src)])
+    lines = subprocess.run([str(exe)], capture_output=True, text=True,
+                           check=True).stdout.split("\n")
+    o = rb.rb_options
+    assert list(map(int, lines[0].split())) == [ctypes.sizeof(o), o.weighting.offset,
+                                                 o.budget.offset, o.instance_mask.offset,
+                                                 o.order_out.offset,
+                                                 ctypes.sizeof(rb.rb_instances)]
+    assert list(map(int, lines[1].split())) == [ctypes.sizeof(rb.rb_weights),
+                                                 rb.rb_weights.w_cost.offset]
 
 
 def test_advance_validation():
