@@ -18,6 +18,8 @@ Every function follows the passage named in the C source:
   assign   -- greedy assignment with dead reckoning, in arrival or LPT order,
               over each request's candidate set (Alg. 1, Sec. 4.1-4.2)
   advance  -- drain the state over an inter-batch gap (clamped linear drain)
+  batch_matching -- the exact batch-level matching on a logged score matrix
+              that Sec. 4.1 compares the greedy with (Hungarian method)
 """
 from __future__ import annotations
 
@@ -278,3 +280,43 @@ def advance(p, a, prefill_rate, decode_rate, dt):
     _check(_load().oracle_advance(_ptr(p), _ptr(a), _ptr(P), _ptr(D), p.shape[0], float(dt)),
            "oracle_advance")
     return p, a
+
+
+def batch_matching(S0, capacity):
+    """Exact batch-level matching on a logged batch-start score matrix.
+
+    Sec. 4.1 compares the greedy pass with a batch-level matching (e.g. the
+    Hungarian method) over the logged score matrices: each request goes to
+    one instance, scored at the batch-start state (no within-batch updates),
+    maximising the total score. The paper gives no instance capacity; here
+    instance i offers ``capacity`` slots (an int, or an int array [I]), and
+    the matching is the linear assignment of the B requests to the slots.
+    With capacity >= B it reduces to the row-wise argmax of S0 (lowest
+    instance on ties). Non-finite entries of S0 (non-candidates) are never
+    matched while a finite choice remains.
+
+    Returns int32 [B] instance per request. The assignment step is scipy's
+    linear_sum_assignment (a library primitive for the Hungarian problem).
+    """
+    from scipy.optimize import linear_sum_assignment
+
+    S0 = np.asarray(S0, np.float64)
+    B, I = S0.shape
+    cap = np.broadcast_to(np.asarray(capacity, np.int64), (I,))
+    if np.any(cap < 0) or cap.sum() < B:
+        raise ValueError("the slots must cover the batch")
+    if B == 0:
+        return np.zeros(0, np.int32)
+    if np.all(cap >= B):
+        # every request takes its best instance
+        V = np.where(np.isfinite(S0), S0, -np.inf)
+        return np.argmax(V, axis=1).astype(np.int32)
+    cols = np.repeat(np.arange(I), np.minimum(cap, B))
+    finite = np.isfinite(S0)
+    span = (np.abs(S0[finite]).max() if finite.any() else 1.0) + 1.0
+    # a non-candidate costs more than any total of finite scores can regain
+    V = np.where(finite, S0, -(2.0 * span * (B + 1)))
+    rows, c = linear_sum_assignment(-V[:, cols])
+    out = np.empty(B, np.int32)
+    out[rows] = cols[c]
+    return out

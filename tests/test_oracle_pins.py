@@ -536,3 +536,54 @@ def test_budget_filter_invariants(seed):
         np.testing.assert_allclose(r["p"][i] - inst.prefill_q[i], pl[sel].sum(), rtol=1e-12)
         np.testing.assert_allclose(r["a"][i] - inst.decode_q[i],
                                    lh[sel, inst.model[i]].sum(), rtol=1e-12, atol=1e-9)
+
+
+# ----------------------------------------------------------------------------- batch matching
+
+
+def _brute_matching(S0, cap):
+    """All I^B assignments within the capacities; the best total and its argmax."""
+    import itertools
+    B, I = S0.shape
+    best, arg = -np.inf, None
+    for a in itertools.product(range(I), repeat=B):
+        if np.any(np.bincount(a, minlength=I) > cap):
+            continue
+        v = S0[np.arange(B), a].sum()
+        if v > best:
+            best, arg = v, a
+    return best, np.array(arg)
+
+
+def test_batch_matching_hand_example():
+    # two requests, two one-slot instances: taking 0.9 forces 0.1 (total 1.0),
+    # the matching takes 0.8 + 0.85 = 1.65; without capacity both pick i0
+    S0 = np.array([[0.9, 0.8], [0.85, 0.1]])
+    assert oracle.batch_matching(S0, 1).tolist() == [1, 0]
+    assert oracle.batch_matching(S0, 2).tolist() == [0, 0]
+    # a non-candidate (NaN) is never matched while a finite choice remains
+    S1 = np.array([[np.nan, 0.2], [0.3, 0.9]])
+    assert oracle.batch_matching(S1, 1).tolist() == [1, 0]
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_batch_matching_matches_brute_force(seed):
+    rng = np.random.default_rng(500 + seed)
+    B, I = 6, 3
+    S0 = rng.uniform(0, 1, (B, I))
+    for cap in (2, 3, np.array([1, 2, 3]), np.array([4, 1, 1])):
+        best, arg = _brute_matching(S0, np.broadcast_to(cap, (I,)))
+        got = oracle.batch_matching(S0, cap)
+        assert np.all(np.bincount(got, minlength=I) <= np.broadcast_to(cap, (I,)))
+        np.testing.assert_allclose(S0[np.arange(B), got].sum(), best, rtol=1e-12)
+        assert got.tolist() == arg.tolist()        # continuous scores: the optimum is unique
+
+
+def test_batch_matching_without_capacity_is_row_argmax():
+    rng = np.random.default_rng(7)
+    S0 = rng.uniform(0, 1, (40, 5))
+    S0[3, 1] = S0[3, 4] = 2.0                      # a tie: the lower instance
+    got = oracle.batch_matching(S0, 40)
+    assert got.tolist() == np.argmax(S0, axis=1).tolist()
+    with pytest.raises(ValueError):
+        oracle.batch_matching(S0, 7)               # 5 x 7 slots < 40 requests
