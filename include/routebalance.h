@@ -106,8 +106,9 @@ typedef struct {
 /* Human-readable name of a status code (static storage, never NULL). */
 const char *rb_status_string(rb_status s);
 
-/* Bytes of device workspace that rb_knn_topk and rb_route_batch need for these
- * sizes on the current device, written to *bytes (a host pointer). The value
+/* Bytes of device workspace that rb_knn_topk, rb_knn_predict, rb_route_batch and
+ * rb_route_batch_ex need for these sizes on the current device (with or without
+ * RB_FLAG_OVERLAP), written to *bytes (a host pointer). The value
  * depends on the device's compute-unit count; query it on the device that will
  * run the call. Errors: RB_ERR_NULL (bytes), RB_ERR_DIMS / RB_ERR_DTYPE as for
  * rb_knn_topk, RB_ERR_HIP if the device cannot be queried. */
@@ -188,9 +189,21 @@ rb_status rb_assign(const float *q_hat, const float *l_hat, const int32_t *promp
                     int M, const rb_instances *inst, int I, rb_weights w, int32_t *assign,
                     float *chosen_score, void *stream);
 
-/* Options of rb_assign_ex and rb_route_batch_ex (a host struct; the pointers
- * are device pointers). A zero-initialised struct (or a NULL options pointer)
- * gives the defaults, under which the _ex calls behave as the plain ones.
+/* Flags of rb_options.
+ *   RB_FLAG_OVERLAP: the bank scan of rb_knn_predict / rb_route_batch_ex
+ *     leaves a compute unit free on each XCD so that a greedy pass
+ *     (rb_assign_ex) of another batch, enqueued on another stream, runs beside
+ *     it instead of waiting for the scan to drain. The scan's rows are spread
+ *     over the remaining units (3 % fewer on MI355X for a batch of up to 256
+ *     requests, more for larger batches, whose query tiles share an XCD; a
+ *     bank whose rows per unit would pass 2 GB is split further and may
+ *     leave none free). Results do not change. */
+#define RB_FLAG_OVERLAP 1u
+
+/* Options of rb_assign_ex, rb_knn_predict and rb_route_batch_ex (a host
+ * struct; the pointers are device pointers). A zero-initialised struct (or a
+ * NULL options pointer) gives the defaults, under which the _ex calls behave
+ * as the plain ones.
  *   order          processing order of the greedy loop (rb_order).
  *   weighting      neighbour averaging (rb_knn_weighting); read by
  *                  rb_route_batch_ex only.
@@ -204,6 +217,7 @@ rb_status rb_assign(const float *q_hat, const float *l_hat, const int32_t *promp
  *                  order_out[t] = request decided at step t. Required by
  *                  rb_assign_ex when order is RB_ORDER_LPT (it also serves as
  *                  that call's scratch); optional for rb_route_batch_ex.
+ *   flags          RB_FLAG_* bits; other bits must be 0.
  * The candidate set of a request is the available, admitted instances; Eq. 1's
  * cost and latency maxima run over it (Sec. 4.1: normalised by the candidates'
  * maxima) and the argmax is taken within it. A request with an empty candidate
@@ -214,6 +228,7 @@ typedef struct {
     const float *budget;
     const uint8_t *instance_mask;
     int32_t *order_out;
+    uint32_t flags;
 } rb_options;
 
 /* rb_assign with options (Alg. 1 with its LPT order and budget filter, and an
@@ -238,6 +253,25 @@ rb_status rb_route_batch(const void *queries, const void *bank, const float *ban
                          const rb_instances *inst, int I, rb_weights w, int32_t *assign,
                          float *chosen_score, int32_t *nbr_idx, float *nbr_dist, float *q_hat,
                          float *l_hat, void *ws, size_t ws_bytes, void *stream);
+
+/* The estimation half of the path for one batch (Alg. 1's one batched KNN
+ * lookup): rb_knn_topk, then the label average of opts->weighting, in one
+ * call. Nothing here reads the instance state, so the lookup of the next
+ * batch can run on one stream while rb_assign_ex decides the current batch on
+ * another (with RB_FLAG_OVERLAP the scan leaves room for it).
+ *   q_hat, l_hat [B][M] fp32 (outputs, required); nbr_idx, nbr_dist [B][k]
+ *   (outputs, may be NULL: then kept in the workspace); opts may be NULL; its
+ *   order, budget, instance_mask and order_out are not read.
+ *   ws: as for rb_route_batch (rb_workspace_size bytes); the call uses only
+ *   its own workspace, so concurrent calls need distinct workspaces.
+ * Errors: as rb_knn_topk, plus RB_ERR_DIMS (M < 1, M > RB_MAX_M), RB_ERR_NULL
+ * (bank_qual, bank_len, q_hat, l_hat), RB_ERR_UNSUPPORTED (weighting or
+ * flags out of range). */
+rb_status rb_knn_predict(const void *queries, const void *bank, const float *bank_norms,
+                         rb_dtype dtype, int B, int N, int d, int k, const float *bank_qual,
+                         const float *bank_len, int M, const rb_options *opts, int32_t *nbr_idx,
+                         float *nbr_dist, float *q_hat, float *l_hat, void *ws, size_t ws_bytes,
+                         void *stream);
 
 /* rb_route_batch with options: the averaging rule of opts->weighting, then
  * rb_assign_ex's order, budgets and mask. The workspace is the same size as

@@ -25,12 +25,13 @@ RB_ERR_WORKSPACE, RB_ERR_UNSUPPORTED, RB_ERR_HIP, RB_ERR_ALIGN = -5, -6, -7, -8
 RB_F32, RB_BF16 = 0, 1
 RB_KNN_UNIFORM, RB_KNN_INV_DIST = 0, 1
 RB_ORDER_ARRIVAL, RB_ORDER_LPT = 0, 1
+RB_FLAG_OVERLAP = 1
 RB_MAX_K, RB_MAX_D, RB_MAX_I, RB_MAX_M = 64, 2048, 1024, 1024
 
 # every symbol include/routebalance.h declares
 EXPORTS = ("rb_status_string", "rb_workspace_size", "rb_bank_norms", "rb_knn_topk", "rb_predict",
-           "rb_score", "rb_assign", "rb_assign_ex", "rb_route_batch", "rb_route_batch_ex",
-           "rb_advance_state", "rb_profile_scan_events")
+           "rb_score", "rb_assign", "rb_assign_ex", "rb_knn_predict", "rb_route_batch",
+           "rb_route_batch_ex", "rb_advance_state", "rb_profile_scan_events")
 
 
 class RbError(RuntimeError):
@@ -52,7 +53,8 @@ class rb_instances(ctypes.Structure):
 
 class rb_options(ctypes.Structure):
     _fields_ = [("order", ctypes.c_int), ("weighting", ctypes.c_int), ("budget", ctypes.c_void_p),
-                ("instance_mask", ctypes.c_void_p), ("order_out", ctypes.c_void_p)]
+                ("instance_mask", ctypes.c_void_p), ("order_out", ctypes.c_void_p),
+                ("flags", ctypes.c_uint32)]
 
 
 def _load():
@@ -71,6 +73,8 @@ def _load():
         "rb_assign": ([P, P, P, i, i, ctypes.POINTER(rb_instances), i, rb_weights, P, P, P], st),
         "rb_assign_ex": ([P, P, P, i, i, ctypes.POINTER(rb_instances), i, rb_weights,
                           ctypes.POINTER(rb_options), P, P, P], st),
+        "rb_knn_predict": ([P, P, P, i, i, i, i, i, P, P, i, ctypes.POINTER(rb_options), P, P, P,
+                            P, P, sz, P], st),
         "rb_route_batch": ([P, P, P, i, i, i, i, i, P, P, i, P, ctypes.POINTER(rb_instances), i,
                             rb_weights, P, P, P, P, P, P, P, sz, P], st),
         "rb_route_batch_ex": ([P, P, P, i, i, i, i, i, P, P, i, P, ctypes.POINTER(rb_instances),
@@ -289,7 +293,7 @@ def rb_route_batch(queries, bank, bank_norms, k: int, bank_qual, bank_len, promp
 
 def options(order: int = RB_ORDER_ARRIVAL, weighting: int = RB_KNN_UNIFORM,
             budget: Optional[torch.Tensor] = None, instance_mask: Optional[torch.Tensor] = None,
-            order_out: Optional[torch.Tensor] = None) -> rb_options:
+            order_out: Optional[torch.Tensor] = None, flags: int = 0) -> rb_options:
     """An rb_options struct; budget fp32 [B], instance_mask uint8 [I], order_out int32 [B].
 
     The struct holds references to the tensors, so their memory stays
@@ -300,7 +304,7 @@ def options(order: int = RB_ORDER_ARRIVAL, weighting: int = RB_KNN_UNIFORM,
         if t is not None and t.dtype != dt:
             raise ValueError(f"{name}: expected {dt}, got {t.dtype}")
     o = rb_options(int(order), int(weighting), _ptr(budget), _ptr(instance_mask),
-                   _ptr(order_out))
+                   _ptr(order_out), int(flags))
     o._tensors = (budget, instance_mask, order_out)
     return o
 
@@ -329,6 +333,30 @@ def rb_assign_ex(q_hat, l_hat, prompt_len, inst: DeviceInstances, weights, opts:
                              inst.I, _w(weights), ctypes.byref(opts), _ptr(assign), _ptr(chosen),
                              _stream(stream)), "rb_assign_ex")
     return assign, chosen
+
+
+def rb_knn_predict(queries, bank, bank_norms, k: int, bank_qual, bank_len,
+                   opts: Optional[rb_options] = None, ws: Optional[torch.Tensor] = None,
+                   q_hat: Optional[torch.Tensor] = None, l_hat: Optional[torch.Tensor] = None,
+                   nbr_idx: Optional[torch.Tensor] = None, nbr_dist: Optional[torch.Tensor] = None,
+                   stream=None):
+    """KNN lookup and label average in one call: returns (q_hat, l_hat)."""
+    B, d = queries.shape
+    N = bank.shape[0]
+    M = bank_qual.shape[1]
+    dev = queries.device
+    if q_hat is None:
+        q_hat = torch.empty(B, M, dtype=torch.float32, device=dev)
+    if l_hat is None:
+        l_hat = torch.empty(B, M, dtype=torch.float32, device=dev)
+    if ws is None:
+        ws = workspace(B, N, d, _dtype_code(bank), k, M, dev)
+    _check(_lib.rb_knn_predict(_ptr(queries), _ptr(bank), _ptr(bank_norms), _dtype_code(bank), B,
+                               N, d, k, _ptr(bank_qual), _ptr(bank_len), M,
+                               ctypes.byref(opts) if opts is not None else None, _ptr(nbr_idx),
+                               _ptr(nbr_dist), _ptr(q_hat), _ptr(l_hat), _ptr(ws), ws.numel(),
+                               _stream(stream)), "rb_knn_predict")
+    return q_hat, l_hat
 
 
 def rb_route_batch_ex(queries, bank, bank_norms, k: int, bank_qual, bank_len, prompt_len,

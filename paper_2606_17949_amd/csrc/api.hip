@@ -119,13 +119,16 @@ RouteExtra route_extra(size_t base, int B, int k, int M)
     return e;
 }
 
-const rb_options k_default_opts = {RB_ORDER_ARRIVAL, RB_KNN_UNIFORM, nullptr, nullptr, nullptr};
+const rb_options k_default_opts = {RB_ORDER_ARRIVAL, RB_KNN_UNIFORM, nullptr, nullptr, nullptr,
+                                   0u};
 
 rb_status check_opts(const rb_options *o)
 {
     if (o->order != RB_ORDER_ARRIVAL && o->order != RB_ORDER_LPT)
         return RB_ERR_UNSUPPORTED;
     if (o->weighting != RB_KNN_UNIFORM && o->weighting != RB_KNN_INV_DIST)
+        return RB_ERR_UNSUPPORTED;
+    if (o->flags & ~RB_FLAG_OVERLAP)
         return RB_ERR_UNSUPPORTED;
     return RB_OK;
 }
@@ -150,12 +153,17 @@ hipError_t enqueue_assign(const float *qh, const float *lh, const int32_t *plen,
                              ao, assign, chosen, st);
 }
 
-rb_status plan(int B, int N, int d, rb_dtype dt, int k, rb::KnnPlan *p)
+// The KNN plan on the current device. With `overlap`, the scan leaves one
+// compute unit of each XCD free, so that a single-workgroup kernel of another
+// stream (the greedy pass, the carry) finds room on whichever XCD it is
+// dispatched to instead of waiting for the scan to drain.
+// rb_workspace_size covers both plans.
+rb_status plan(int B, int N, int d, rb_dtype dt, int k, rb::KnnPlan *p, bool overlap = false)
 {
     int cu = 0;
     if (num_cu(&cu) != 0)
         return RB_ERR_HIP;
-    if (rb::plan_knn(B, N, d, (int)dt, k, cu, p) != 0)
+    if (rb::plan_knn(B, N, d, (int)dt, k, cu, p, overlap ? 1 : 0) != 0)
         return RB_ERR_DIMS;
     return RB_OK;
 }
@@ -187,7 +195,7 @@ rb_status route_batch(const void *queries, const void *bank, const float *bank_n
     if (!aligned(queries, 16) || !aligned(bank, 16))
         return RB_ERR_ALIGN;
     rb::KnnPlan p;
-    if ((s = plan(B, N, d, dtype, k, &p)) != RB_OK)
+    if ((s = plan(B, N, d, dtype, k, &p, (o->flags & RB_FLAG_OVERLAP) != 0)) != RB_OK)
         return s;
     const RouteExtra ex = route_extra(p.bytes, B, k, M);
     if (!ws || ws_bytes < ex.bytes)
@@ -239,10 +247,12 @@ rb_status rb_workspace_size(int B, int N, int d, rb_dtype dtype, int k, int M, s
         return s;
     if (M < 1 || M > RB_MAX_M)
         return RB_ERR_DIMS;
-    rb::KnnPlan p;
+    rb::KnnPlan p, q;
     if ((s = plan(B, N, d, dtype, k, &p)) != RB_OK)
         return s;
-    *bytes = route_extra(p.bytes, B, k, M).bytes;
+    if ((s = plan(B, N, d, dtype, k, &q, true)) != RB_OK)
+        return s;
+    *bytes = route_extra(p.bytes > q.bytes ? p.bytes : q.bytes, B, k, M).bytes;
     return RB_OK;
 }
 
@@ -366,6 +376,40 @@ rb_status rb_assign_ex(const float *q_hat, const float *l_hat, const int32_t *pr
     if (e == hipSuccess && o->order != RB_ORDER_LPT && o->order_out)
         e = rb::launch_iota(o->order_out, B, st);
     return hip_status(e);
+}
+
+rb_status rb_knn_predict(const void *queries, const void *bank, const float *bank_norms,
+                         rb_dtype dtype, int B, int N, int d, int k, const float *bank_qual,
+                         const float *bank_len, int M, const rb_options *opts, int32_t *nbr_idx,
+                         float *nbr_dist, float *q_hat, float *l_hat, void *ws, size_t ws_bytes,
+                         void *stream)
+{
+    const rb_options *o = opts ? opts : &k_default_opts;
+    rb_status s = check_knn_dims(dtype, B, N, d, k);
+    if (s != RB_OK)
+        return s;
+    if (M < 1 || M > RB_MAX_M)
+        return RB_ERR_DIMS;
+    if ((s = check_opts(o)) != RB_OK)
+        return s;
+    if (B == 0)
+        return RB_OK;
+    if (!queries || !bank || !bank_norms || !bank_qual || !bank_len || !q_hat || !l_hat)
+        return RB_ERR_NULL;
+    if (!aligned(queries, 16) || !aligned(bank, 16))
+        return RB_ERR_ALIGN;
+    rb::KnnPlan p;
+    if ((s = plan(B, N, d, dtype, k, &p, (o->flags & RB_FLAG_OVERLAP) != 0)) != RB_OK)
+        return s;
+    const RouteExtra ex = route_extra(p.bytes, B, k, M);
+    if (!ws || ws_bytes < ex.bytes)
+        return RB_ERR_WORKSPACE;
+    if (!aligned(ws, 256))
+        return RB_ERR_ALIGN;
+    int32_t *nbr = nbr_idx ? nbr_idx : (int32_t *)((uint8_t *)ws + ex.off_nbr);
+    return hip_status(rb::launch_knn(p, queries, bank, bank_norms, ws, nbr, nbr_dist, bank_qual,
+                                     bank_len, M, q_hat, l_hat,
+                                     o->weighting == RB_KNN_INV_DIST, (hipStream_t)stream));
 }
 
 rb_status rb_route_batch(const void *queries, const void *bank, const float *bank_norms,

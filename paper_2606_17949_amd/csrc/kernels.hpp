@@ -7,27 +7,31 @@
 
 namespace rb {
 
-constexpr int SCAN_THREADS = 256;   // 4 waves, one per SIMD
-constexpr int SCAN_WAVES = 4;
-constexpr int SCAN_RT = 3;         // 16-row MFMA tiles per wave per iteration (48 rows)
-constexpr int SCAN_PREFETCH = 3;    // k-steps whose loads are in flight ahead of the MFMAs
-constexpr int SCAN_UNROLL = 4;      // register ring of bank fragments; k-steps are padded to it
-constexpr int STAGE_CAP = 256;      // per-wave LDS staging of one iteration's candidates
+// The scan runs 8 waves, two per SIMD, each within half the register file
+// (256 registers: 128 accumulators for 2 row tiles x 16 query groups): the
+// workgroup covers 256 bank rows per iteration, so every streamed query byte
+// serves 256 rows, and each SIMD has a second wave to cover load latency.
+constexpr int SCAN_THREADS = 512;   // 8 waves, two per SIMD
+constexpr int SCAN_WAVES = 8;
+constexpr int SCAN_RT = 2;          // 16-row MFMA tiles per wave per iteration (32 rows)
+constexpr int SCAN_PREFETCH = 1;    // k-steps whose loads are in flight ahead of the MFMAs
+constexpr int SCAN_UNROLL = 2;      // register ring of bank fragments; k-steps are padded to it
+constexpr int STAGE_CAP = 128;      // per-wave LDS staging of one iteration's candidates
 constexpr size_t LDS_LIMIT = 160 * 1024;
 constexpr int MERGE_WAVES = 4;      // queries per merge workgroup, one wave each
 constexpr int MERGE_CAP = 2048;     // candidates per query the merge holds in LDS
 constexpr int MERGE_MAX_LISTS = 64 * 64;   // 64 lists per lane
 constexpr int RB_MAX_K_DEV = 64;    // largest k (the ABI limit)
-constexpr int SEED_MAX_GROUPS = 512;   // S / 64 for S <= 32768
+constexpr int SEED_MAX_GROUPS = 2048;  // S / 16 for S <= 32768
 
 // How one rb_knn_topk call is split.
 //  * seed: S bank rows spread evenly over the bank; per query, the k-th
-//    smallest of the S/64 minima over groups of 64 of them bounds the k-th
+//    smallest of the S/16 minima over groups of 16 of them bounds the k-th
 //    nearest distance from above (k distinct rows lie at or below it).
 //  * scan: query tiles of 16*ng queries, whose first gr groups stay in LDS
 //    for the whole call while the others stream through it; the
 //    bank in n_chunks contiguous row ranges (multiples of 16 rows); one
-//    workgroup per (chunk, tile); each of its 4 waves owns 16*rt rows per
+//    workgroup per (chunk, tile); each of its SCAN_WAVES waves owns 16*rt rows per
 //    iteration; the workgroup keeps, per query, one list of the k best
 //    candidates that pass the bound.
 //  * merge: per query, the k smallest of its W = n_chunks lists.
@@ -45,7 +49,8 @@ struct KnnPlan {
     size_t off_tau, off_qn, off_gmin, off_ccnt, off_ckey, off_cidx, off_ovf, bytes;
 };
 
-int plan_knn(int B, int N, int d, int dtype, int k, int num_cu, KnnPlan *p);
+// reserve: compute units per XCD to leave free for kernels of other streams.
+int plan_knn(int B, int N, int d, int dtype, int k, int num_cu, KnnPlan *p, int reserve = 0);
 
 // Events recorded around the bank-scan kernel when set (per host thread).
 void set_scan_events(hipEvent_t begin, hipEvent_t end);

@@ -3,7 +3,7 @@
 //
 // Kernels of one call:
 //   seed_groups_kernel  distances of every query to S bank rows spread evenly
-//                       over the bank; minima over groups of 64 of those rows
+//                       over the bank; minima over groups of 16 of those rows
 //   seed_bound_kernel   per query: |q|^2, and the k-th smallest group minimum
 //                       as the starting bound of the k-th nearest distance
 //   scan_kernel         the bank once through MFMA (scan.hpp): one workgroup
@@ -63,73 +63,115 @@ __device__ __forceinline__ long seed_row(int j, int N, int S)
     return (long)j * N / S;
 }
 
-// One workgroup of 16 waves per group of 64 sample rows; wave w takes query
-// group 16*blockIdx.y + w. Per k-step the 64 rows' 64-byte slices are staged
-// once in an LDS double buffer (one 16-byte load by each of 256 threads), so
-// the 16 waves do not each fetch them; each wave reads the 4 row-tile
-// fragments from LDS and its own query fragment (loaded a k-step ahead) from
-// global memory. p = |x|^2 - 2<q,x> by MFMA; each query keeps the minimum over
-// the 64 rows.
-constexpr int SEED_WAVES = 16;
+// One workgroup of SEED_WAVES waves per SEED_WAVES groups of 16 sample rows
+// and QG query groups of 16 (blockIdx.y): wave w owns group 8*blockIdx.x + w.
+// Its bank fragments (row lane%16 of the group, 16-byte quarter lane/16 of
+// each 64-byte k-step) come straight from global memory, three k-steps ahead;
+// the workgroup stages the k-step's query fragments once in an LDS double
+// buffer, so every query is loaded once per workgroup and every sample row
+// once. p = |x|^2 - 2<q,x> by MFMA (the accumulators start at -|x|^2/2); each
+// query keeps the minimum over the group's 16 rows.
+constexpr int SEED_WAVES = 8;
+constexpr int SEED_RING = 4;   // k-steps of loads in flight (even: LDS buffer = slot parity)
 
-template <int DT>
+template <int DT, int QG>
 __global__ __launch_bounds__(SEED_WAVES * WAVE) void seed_groups_kernel(const SeedArgs A)
 {
     constexpr int VEC = Elem<DT>::VEC, ESZ = Elem<DT>::ESZ;
-    __shared__ i32x4 abuf[2][4][WAVE];   // [buffer][row tile][lane]
+    constexpr int NT = SEED_WAVES * WAVE;
+    constexpr int QPT = (QG * WAVE + NT - 1) / NT;   // query fragments each thread stages
+    __shared__ i32x4 qs[2][QG][WAVE];
     const int tid = threadIdx.x, lane = lane_id(), wave = tid >> 6;
     const int col = lane & 15, jg = lane >> 4;
-    const int sb = blockIdx.x;
-    const int qg = blockIdx.y * SEED_WAVES + wave;
-    const bool wv = qg < A.n_qg;
+    const int grp = blockIdx.x * SEED_WAVES + wave;
+    const bool gv = grp < A.G;
+    const int qg0 = blockIdx.y * QG;
     const size_t rowb = (size_t)A.d * ESZ;
-    const int q = qg * 16 + col;
-    const bool qv = wv && q < A.B;
     const i32x4 z = {0, 0, 0, 0};
-    // staging: thread tid < 256 loads row tile tid/64, lane tid%64 of every k-step
-    const int st_t = (tid >> 6) & 3, st_l = tid & 63;
-    const uint8_t *sp = A.bank + (size_t)seed_row(sb * 64 + st_t * 16 + (st_l & 15), A.N, A.S) * rowb +
-                        (st_l >> 4) * 16;
-    auto stage_load = [&](int s) -> i32x4 {
-        return s * 4 * VEC + (st_l >> 4) * VEC < A.d ? load16(sp + (size_t)s * KSTEP_BYTES) : z;
+    const uint8_t *ap =
+        A.bank + (gv ? (size_t)seed_row(grp * 16 + col, A.N, A.S) * rowb : 0) + jg * 16;
+    auto a_load = [&](int s) -> i32x4 {
+        return gv && s < A.nks && s * 4 * VEC + jg * VEC < A.d ? load16(ap + (size_t)s * KSTEP_BYTES)
+                                                               : z;
     };
-    const uint8_t *qp = A.queries + (qv ? (size_t)q * rowb : 0) + jg * 16;
-    auto query_load = [&](int s) -> i32x4 {
-        return qv && s * 4 * VEC + jg * VEC < A.d ? load16(qp + (size_t)s * KSTEP_BYTES) : z;
-    };
-    f32x4 acc[4];
+    // staged fragment f = tid + NT*u is lane f%64 of query group f/64
+    const uint8_t *qp[QPT];
+    bool qv[QPT];
+    int qj[QPT];
 #pragma unroll
-    for (int t = 0; t < 4; ++t)
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-            acc[t][e] = -0.5f * A.bank_norms[seed_row(sb * 64 + t * 16 + jg * 4 + e, A.N, A.S)];
-    if (tid < 256)
-        abuf[0][st_t][st_l] = stage_load(0);
-    i32x4 b = query_load(0);
-    __syncthreads();
-    for (int s = 0; s < A.nks; ++s) {
-        const bool more = s + 1 < A.nks;
-        const i32x4 an = tid < 256 && more ? stage_load(s + 1) : z;
-        const i32x4 bn = more ? query_load(s + 1) : z;
-#pragma unroll
-        for (int t = 0; t < 4; ++t)
-            acc[t] = mfma_step<DT>(abuf[s & 1][t][lane], b, acc[t]);
-        if (tid < 256 && more)
-            abuf[(s + 1) & 1][st_t][st_l] = an;
-        b = bn;
-        __syncthreads();
+    for (int u = 0; u < QPT; ++u) {
+        const int f = tid + NT * u;
+        const int q = (qg0 + (f >> 6)) * 16 + (f & 15);
+        qv[u] = f < QG * WAVE && q < A.B;
+        qj[u] = (f >> 4) & 3;
+        qp[u] = A.queries + (qv[u] ? (size_t)q * rowb : 0) + qj[u] * 16;
     }
-    float m = INFINITY;
-#pragma unroll
-    for (int t = 0; t < 4; ++t)
+    auto q_load = [&](int u, int s) -> i32x4 {
+        return qv[u] && s * 4 * VEC + qj[u] * VEC < A.d ? load16(qp[u] + (size_t)s * KSTEP_BYTES)
+                                                        : z;
+    };
+    auto q_store = [&](int buf, int u, const i32x4 &v) {
+        const int f = tid + NT * u;
+        if (f < QG * WAVE)
+            qs[buf][f >> 6][f & 63] = v;
+    };
+    f32x4 acc[QG];
+    {
+        f32x4 h;
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-            m = fminf(m, -2.f * acc[t][e]);
-    // lanes col, col+16, col+32, col+48 hold the four row quarters of one query
-    m = fminf(m, __shfl_xor(m, 16));
-    m = fminf(m, __shfl_xor(m, 32));
-    if (qv && jg == 0)
-        A.gmin[(size_t)q * A.G + sb] = m;
+            h[e] = gv ? -0.5f * A.bank_norms[seed_row(grp * 16 + jg * 4 + e, A.N, A.S)] : 0.f;
+#pragma unroll
+        for (int g = 0; g < QG; ++g)
+            acc[g] = h;
+    }
+    // register rings: the loads of k-step s + SEED_RING - 1 are issued at step
+    // s; step s's fragment sits in slot s % SEED_RING (the loop is unrolled by
+    // the ring size, so every slot index is a constant)
+    i32x4 ar[SEED_RING], qr[SEED_RING][QPT];
+    static_for<0, SEED_RING - 1>([&](auto J) {
+        ar[J.value] = a_load(J.value);
+#pragma unroll
+        for (int u = 0; u < QPT; ++u)
+            qr[J.value][u] = q_load(u, J.value);
+    });
+#pragma unroll
+    for (int u = 0; u < QPT; ++u)
+        q_store(0, u, qr[0][u]);
+    __syncthreads();
+    for (int s0 = 0; s0 < A.nks; s0 += SEED_RING) {
+        static_for<0, SEED_RING>([&](auto R) {
+            constexpr int r = R.value, nx = (r + SEED_RING - 1) % SEED_RING;
+            const int s = s0 + r;
+            if (s >= A.nks)
+                return;
+            ar[nx] = a_load(s + SEED_RING - 1);
+#pragma unroll
+            for (int u = 0; u < QPT; ++u)
+                qr[nx][u] = q_load(u, s + SEED_RING - 1);
+#pragma unroll
+            for (int g = 0; g < QG; ++g)
+                acc[g] = mfma_step<DT>(ar[r], qs[r & 1][g][lane], acc[g]);
+            if (s + 1 < A.nks) {
+#pragma unroll
+                for (int u = 0; u < QPT; ++u)
+                    q_store((r + 1) & 1, u, qr[(r + 1) % SEED_RING][u]);
+            }
+            __syncthreads();
+        });
+    }
+#pragma unroll
+    for (int g = 0; g < QG; ++g) {
+        // p = -2 * acc for this lane's four rows of the group
+        float m = fminf(fminf(-2.f * acc[g][0], -2.f * acc[g][1]),
+                        fminf(-2.f * acc[g][2], -2.f * acc[g][3]));
+        // lanes col, col+16, col+32, col+48 hold the four row quarters
+        m = fminf(m, __shfl_xor(m, 16));
+        m = fminf(m, __shfl_xor(m, 32));
+        const int q = (qg0 + g) * 16 + col;
+        if (gv && jg == 0 && q < A.B)
+            A.gmin[(size_t)q * A.G + grp] = m;
+    }
 }
 
 // One wave per query: |q|^2, and the starting bound = |q|^2 + the k-th smallest
@@ -153,11 +195,14 @@ __global__ __launch_bounds__(256) void seed_bound_kernel(const uint8_t *__restri
     s = wave_sum(s);
     uint32_t T = KEY_NONE;
     if (G >= k) {
+        // every load in flight at once: lanes past G read the last group and
+        // discard it
         uint32_t key[GPL];
 #pragma unroll
         for (int u = 0; u < GPL; ++u) {
             const int i = lane + WAVE * u;
-            key[u] = i < G ? f2key(gmin[(size_t)b * G + i]) : KEY_NONE;
+            const float v = gmin[(size_t)b * G + (i < G ? i : G - 1)];
+            key[u] = f2key(v) | (i < G ? 0u : KEY_NONE);   // uses v unconditionally
         }
         uint32_t prefix = 0;
         for (int bit = 31; bit >= 0; --bit) {
@@ -406,7 +451,7 @@ void set_scan_events(hipEvent_t begin, hipEvent_t end)
     t_scan_end = end;
 }
 
-int plan_knn(int B, int N, int d, int dtype, int k, int num_cu, KnnPlan *p)
+int plan_knn(int B, int N, int d, int dtype, int k, int num_cu, KnnPlan *p, int reserve)
 {
     const int vec = dtype == 1 ? 8 : 4;
     p->dtype = dtype;
@@ -444,8 +489,16 @@ int plan_knn(int B, int N, int d, int dtype, int k, int num_cu, KnnPlan *p)
     p->rt = SCAN_RT;
     const int bm = p->ng * 16;
     p->n_qt = B > 0 ? (B + bm - 1) / bm : 1;
-    // one workgroup per compute unit (the LDS use allows no more)
+    // one workgroup per compute unit (the LDS use allows no more); with
+    // `reserve`, that many units of each XCD stay free: workgroups go to the
+    // XCDs round robin and the tiles of a chunk share its XCD, so a whole
+    // number of chunks per XCD is kept below the XCD's unit count
     long chunks = num_cu / p->n_qt;
+    if (reserve > 0) {
+        const long per_xcd = (num_cu / 8 - reserve) / p->n_qt;
+        if (per_xcd >= 1)
+            chunks = per_xcd * 8;
+    }
     if (chunks < 1)
         chunks = 1;
     const long max_chunks = ((long)N + 15) / 16;
@@ -475,10 +528,10 @@ int plan_knn(int B, int N, int d, int dtype, int k, int num_cu, KnnPlan *p)
     if (S > N)
         S = N;
     S = S / 64 * 64;
-    if (S / 64 < k)
+    if (S / 16 < k)
         S = 0;
     p->S = (int)S;
-    p->G = (int)(S / 64);
+    p->G = (int)(S / 16);
     size_t off = 0;
     p->off_tau = off;
     off += align256((size_t)B * 4);
@@ -546,11 +599,21 @@ hipError_t launch_knn(const KnnPlan &p, const void *queries, const void *bank,
         sa.G = p.G;
         sa.n_qg = (p.B + 15) / 16;
         sa.gmin = gmin;
-        const dim3 grid(p.S / 64, (sa.n_qg + SEED_WAVES - 1) / SEED_WAVES);
-        if (p.dtype == 1)
-            hipLaunchKernelGGL(seed_groups_kernel<1>, grid, dim3(SEED_WAVES * WAVE), 0, s, sa);
-        else
-            hipLaunchKernelGGL(seed_groups_kernel<0>, grid, dim3(SEED_WAVES * WAVE), 0, s, sa);
+        // 16 query groups per workgroup, or 4 for a batch of at most 64
+        const int qg = sa.n_qg <= 4 ? 4 : 16;
+        const dim3 grid((p.G + SEED_WAVES - 1) / SEED_WAVES, (sa.n_qg + qg - 1) / qg);
+        const dim3 block(SEED_WAVES * WAVE);
+        if (p.dtype == 1) {
+            if (qg == 4)
+                hipLaunchKernelGGL((seed_groups_kernel<1, 4>), grid, block, 0, s, sa);
+            else
+                hipLaunchKernelGGL((seed_groups_kernel<1, 16>), grid, block, 0, s, sa);
+        } else {
+            if (qg == 4)
+                hipLaunchKernelGGL((seed_groups_kernel<0, 4>), grid, block, 0, s, sa);
+            else
+                hipLaunchKernelGGL((seed_groups_kernel<0, 16>), grid, block, 0, s, sa);
+        }
         if ((e = hipGetLastError()) != hipSuccess)
             return e;
     }

@@ -20,17 +20,19 @@ __device__ __forceinline__ uint64_t lds_load64(const uint64_t *p)
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
-// One workgroup per (bank chunk, tile of 16*NG queries); 4 waves, one per SIMD.
-// Each wave owns 16*RT consecutive rows of every 64*RT-row iteration and holds
-// their inner products with all tile queries in MFMA accumulators. Bank rows go
-// from HBM straight into MFMA operand registers (a ring of R k-steps, loads P
-// k-steps ahead). Query fragments come from LDS: the first GR query groups of
-// the tile stay resident for the whole kernel; the other groups stream through
-// a double buffer one k-step at a time (staged through registers two k-steps
-// ahead), and only they need a workgroup barrier per k-step. Candidates that pass
-// a register-level test against the per-query bound go through per-wave staging
-// into one list of the k best per query shared by the workgroup, maintained
-// with 64-bit compare-and-swap so that the four waves insert without locks.
+// One workgroup per (bank chunk, tile of 16*NG queries); SCAN_WAVES waves, two
+// per SIMD. Each wave owns 16*RT consecutive rows of every
+// SCAN_WAVES*16*RT-row iteration and holds their inner products with all tile
+// queries in MFMA accumulators. Bank rows go from HBM straight into MFMA
+// operand registers (a ring of R k-steps, loads P k-steps ahead; the SIMD's
+// other wave covers the rest of the latency). Query fragments come from LDS:
+// the first GR query groups of the tile stay resident for the whole kernel;
+// the other groups stream through a double buffer one k-step at a time
+// (staged through registers two k-steps ahead), and only they need a
+// workgroup barrier per k-step. Candidates that pass a register-level test
+// against the per-query bound go through per-wave staging into one list of
+// the k best per query shared by the workgroup, maintained with 64-bit
+// compare-and-swap so that the waves insert without locks.
 template <int DT, int NG, int GR, int RT, bool RAGGED>
 __global__ __launch_bounds__(SCAN_THREADS, 1) void scan_kernel(const ScanArgs A)
 {

@@ -208,15 +208,36 @@ def test_route_batch_ex_validation():
                 asg=None) == rb.RB_OK
 
 
+def test_knn_predict_validation():
+    def call(opts=None, **kw):
+        a = dict(q=FAKE, B=4, N=100, d=64, k=10, M=4, qual=FAKE, qh=FAKE, lh=FAKE, ws=FAKE)
+        a.update(kw)
+        return L.rb_knn_predict(a["q"], FAKE, FAKE, rb.RB_BF16, a["B"], a["N"], a["d"], a["k"],
+                                a["qual"], FAKE, a["M"], None if opts is None else ctypes.byref(opts),
+                                None, None, a["qh"], a["lh"], a["ws"], 1 << 20, None)
+    assert call(k=0) == rb.RB_ERR_DIMS
+    assert call(M=0) == rb.RB_ERR_DIMS
+    assert call(d=60) == rb.RB_ERR_DIMS
+    assert call(qh=None) == rb.RB_ERR_NULL
+    assert call(lh=None) == rb.RB_ERR_NULL
+    assert call(qual=None) == rb.RB_ERR_NULL
+    assert call(q=MISALIGNED) == rb.RB_ERR_ALIGN
+    assert call(rb.rb_options(0, 2, None, None, None, 0)) == rb.RB_ERR_UNSUPPORTED
+    assert call(rb.rb_options(0, 0, None, None, None, 2)) == rb.RB_ERR_UNSUPPORTED   # unknown flag
+    assert call(rb.rb_options(0, 0, None, None, None, rb.RB_FLAG_OVERLAP), B=0, q=None, qh=None,
+                lh=None, ws=None) == rb.RB_OK
+
+
 def test_struct_layouts_match_the_header(tmp_path):
     # the C compiler's layout of the header's structs against the binding's
     src = tmp_path / "layout.c"
     src.write_text(
         '#include <stdio.h>\n#include <stddef.h>\n#include "routebalance.h"\n'
         'int main(void) {\n'
-        '  printf("%zu %zu %zu %zu %zu %zu\\n", sizeof(rb_options), offsetof(rb_options, weighting),\n'
-        '         offsetof(rb_options, budget), offsetof(rb_options, instance_mask),\n'
-        '         offsetof(rb_options, order_out), sizeof(rb_instances));\n'
+        '  printf("%zu %zu %zu %zu %zu %zu %zu\\n", sizeof(rb_options),\n'
+        '         offsetof(rb_options, weighting), offsetof(rb_options, budget),\n'
+        '         offsetof(rb_options, instance_mask), offsetof(rb_options, order_out),\n'
+        '         offsetof(rb_options, flags), sizeof(rb_instances));\n'
         '  printf("%zu %zu\\n", sizeof(rb_weights), offsetof(rb_weights, w_cost));\n'
         '  return 0;\n}\n')
     exe = tmp_path / "layout"
@@ -227,7 +248,7 @@ def test_struct_layouts_match_the_header(tmp_path):
     o = rb.rb_options
     assert list(map(int, lines[0].split())) == [ctypes.sizeof(o), o.weighting.offset,
                                                  o.budget.offset, o.instance_mask.offset,
-                                                 o.order_out.offset,
+                                                 o.order_out.offset, o.flags.offset,
                                                  ctypes.sizeof(rb.rb_instances)]
     assert list(map(int, lines[1].split())) == [ctypes.sizeof(rb.rb_weights),
                                                  rb.rb_weights.w_cost.offset]
