@@ -26,7 +26,9 @@
  *   - Faults inside kernels surface at the caller's next synchronisation.
  *   - Values that live in device memory are not checked (documented
  *     preconditions): rates > 0, prices >= 0, prompt lengths >= 1, model ids in
- *     [0, M), embeddings, norms and labels finite. Violating them is undefined.
+ *     [0, M), queued prefill and active decode >= 0, quality labels in [0, 1],
+ *     length labels >= 0, embeddings and norms finite. Violating them is
+ *     undefined.
  *   - Results are deterministic: the same inputs give bit-identical outputs on
  *     every call.
  */

@@ -174,19 +174,24 @@ __global__ __launch_bounds__(SEED_WAVES * WAVE) void seed_groups_kernel(const Se
     }
 }
 
-// One wave per query: |q|^2, and the starting bound = |q|^2 + the k-th smallest
-// group minimum, widened by a margin far above any fp32 rounding difference
-// between this pass and the scan. Without a seed (G < k) the bound is +inf.
+// One workgroup of SEED_BOUND_WAVES waves per query: |q|^2, and the starting
+// bound = |q|^2 + the k-th smallest group minimum, widened by a margin far
+// above any fp32 rounding difference between this pass and the scan. The
+// k-th smallest is found bit by bit from the top: each wave counts its share
+// of the group minima below the trial value, and the workgroup adds the four
+// counts through LDS (one barrier per bit). Without a seed (G < k) the bound
+// is +inf.
+constexpr int SEED_BOUND_WAVES = 4;
+
 template <int DT, int GPL>
-__global__ __launch_bounds__(256) void seed_bound_kernel(const uint8_t *__restrict__ queries, int B,
-                                                         int d, int k, const float *__restrict__ gmin,
-                                                         int G, float *__restrict__ qn,
-                                                         uint32_t *__restrict__ tau)
+__global__ __launch_bounds__(SEED_BOUND_WAVES * WAVE) void seed_bound_kernel(
+    const uint8_t *__restrict__ queries, int B, int d, int k, const float *__restrict__ gmin,
+    int G, float *__restrict__ qn, uint32_t *__restrict__ tau)
 {
-    const int lane = lane_id();
-    const int b = (int)(((long)blockIdx.x * blockDim.x + threadIdx.x) >> 6);
-    if (b >= B)
-        return;
+    static_assert(GPL * WAVE * SEED_BOUND_WAVES >= SEED_MAX_GROUPS, "every group has a slot");
+    __shared__ int cnt[2][SEED_BOUND_WAVES];
+    const int lane = lane_id(), wave = threadIdx.x >> 6;
+    const int b = blockIdx.x;
     const int row_bytes = d * Elem<DT>::ESZ;
     const uint8_t *row = queries + (size_t)b * row_bytes;
     float s = 0.f;
@@ -195,12 +200,12 @@ __global__ __launch_bounds__(256) void seed_bound_kernel(const uint8_t *__restri
     s = wave_sum(s);
     uint32_t T = KEY_NONE;
     if (G >= k) {
-        // every load in flight at once: lanes past G read the last group and
+        // every load in flight at once: slots past G read the last group and
         // discard it
         uint32_t key[GPL];
 #pragma unroll
         for (int u = 0; u < GPL; ++u) {
-            const int i = lane + WAVE * u;
+            const int i = (wave * GPL + u) * WAVE + lane;
             const float v = gmin[(size_t)b * G + (i < G ? i : G - 1)];
             key[u] = f2key(v) | (i < G ? 0u : KEY_NONE);   // uses v unconditionally
         }
@@ -211,7 +216,15 @@ __global__ __launch_bounds__(256) void seed_bound_kernel(const uint8_t *__restri
 #pragma unroll
             for (int u = 0; u < GPL; ++u)
                 c += key[u] < trial;
-            if ((int)wave_sum((float)c) < k)
+            const int wc = (int)wave_sum((float)c);
+            if (lane == 0)
+                cnt[bit & 1][wave] = wc;
+            __syncthreads();   // (the other buffer is rewritten only after the next barrier)
+            int total = 0;
+#pragma unroll
+            for (int w = 0; w < SEED_BOUND_WAVES; ++w)
+                total += cnt[bit & 1][w];
+            if (total < k)
                 prefix = trial;
         }
         const float pk = key2f(prefix);
@@ -219,7 +232,7 @@ __global__ __launch_bounds__(256) void seed_bound_kernel(const uint8_t *__restri
         const float margin = ldexpf(s + fabsf(pk) + 1.f, -14);
         T = f2key(t + margin);
     }
-    if (lane == 0) {
+    if (threadIdx.x == 0) {
         qn[b] = s;
         tau[b] = T;
     }
@@ -435,10 +448,10 @@ template <int DT>
 hipError_t launch_seed_bound(const KnnPlan &p, const void *queries, const float *gmin, float *qn,
                              uint32_t *tau, hipStream_t s)
 {
-    const int grid = (p.B + 3) / 4;
     const uint8_t *q = (const uint8_t *)queries;
     const int G = p.S ? p.G : 0;
-    hipLaunchKernelGGL((seed_bound_kernel<DT, SEED_MAX_GROUPS / WAVE>), dim3(grid), dim3(256), 0, s,
+    constexpr int GPL = SEED_MAX_GROUPS / (WAVE * SEED_BOUND_WAVES);
+    hipLaunchKernelGGL((seed_bound_kernel<DT, GPL>), dim3(p.B), dim3(SEED_BOUND_WAVES * WAVE), 0, s,
                        q, p.B, p.d, p.k, gmin, G, qn, tau);
     return hipGetLastError();
 }

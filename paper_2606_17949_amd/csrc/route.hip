@@ -129,16 +129,27 @@ __global__ __launch_bounds__(LPT_THREADS) void lpt_order_kernel(const float *__r
 // instance i = lane % 16, replicated in the four rows of 16 lanes, so every
 // reduction stays inside a row and leaves its result in every lane. WIDTH = 64:
 // instance i = lane + 64*u in register slot u. Per request: the latency
-// maximum (one reduction), the scores, then one reduction of (score key,
-// ~instance) pairs that yields the largest score and, among equal scores, the
-// lowest instance index; the lanes holding that instance update its state.
-// A request without candidates gets -1 and changes no state.
-constexpr int ASSIGN_THREADS = 1024;
-constexpr int ASSIGN_WAVES = ASSIGN_THREADS / WAVE;
+// maximum, then the pick. Latencies are positive (queues and lengths are
+// non-negative, prompts at least one token, rates positive), so the Eq. 1
+// score orders the candidates as S*Tmax = base*Tmax + w_lat*(Tmax - T) does,
+// which needs no division; both T and S*Tmax are non-negative (scores lie in
+// [0, 1]), so their float bits order as unsigned integers, and one more than
+// the bits of S*Tmax is never 0, which marks a non-candidate. One unsigned
+// maximum, a ballot of the lanes that hold it and a find-first-set give the
+// largest score and, among equal scores, the lowest instance index;
+// the lanes holding that instance update its state. The pick's base score,
+// latency and Tmax are captured, one step per lane, and every 64 steps the
+// wave writes the picks and computes their Eq. 1 scores (with the division,
+// exactly as the dense score kernel does) in one vector pass. A request
+// without candidates gets -1 and changes no state.
+// 16 waves; 8 for 16 register slots per lane (more than 512 instances), whose
+// state and scores need the larger register share of a half-size workgroup
+template <int IPL>
+constexpr int assign_threads() { return IPL >= 16 ? 512 : 1024; }
 constexpr int ASSIGN_LDS_FLOATS = 8192;   // per buffer: chunk rows x instances x 2
 
 template <int IPL, int WIDTH>
-__global__ __launch_bounds__(ASSIGN_THREADS) void assign_kernel(
+__global__ __launch_bounds__(assign_threads<IPL>()) void assign_kernel(
     const float *__restrict__ q_hat, const float *__restrict__ l_hat,
     const int32_t *__restrict__ plen, int B, int M, const InstArgs in, int I, float wq, float wl,
     float wc, const AssignOpts opt, int32_t *__restrict__ assign, float *__restrict__ chosen)
@@ -166,7 +177,7 @@ __global__ __launch_bounds__(ASSIGN_THREADS) void assign_kernel(
     // producers: step t = c*CH + j into slot j of buffer c & 1, one wave per step
     auto produce = [&](int c) {
         const int buf = c & 1;
-        for (int j = wave - 1; j < CH; j += ASSIGN_WAVES - 1) {
+        for (int j = wave - 1; j < CH; j += assign_threads<IPL>() / WAVE - 1) {
             const int t = c * CH + j;
             if (t >= B)
                 break;
@@ -233,6 +244,17 @@ __global__ __launch_bounds__(ASSIGN_THREADS) void assign_kernel(
         rP[u] = valid[u] ? 1.f / in.P[i] : 0.f;
         rD[u] = valid[u] ? 1.f / in.D[i] : 0.f;
     }
+    const auto umax = [](uint32_t x, uint32_t y) { return x > y ? x : y; };
+    // maximum over the instance set (every lane of the row, or of the wave)
+    auto umax_all = [&](uint32_t v) {
+        if constexpr (WIDTH == 16)
+            return row16_reduce(v, umax);
+        else
+            return wave_reduce(v, umax);
+    };
+    // captured picks, step (j mod 64) in lane (j mod 64)
+    int cap_i = -1, cap_r = 0;
+    float cap_b = 0.f, cap_t = 0.f, cap_m = 0.f;
     __syncthreads();   // chunk 0 is ready
     for (int c = 0; c < n_ch; ++c) {
         const int buf = c & 1;
@@ -255,38 +277,74 @@ __global__ __launch_bounds__(ASSIGN_THREADS) void assign_kernel(
                 bsn[u] = base_s[buf][jn][col + WAVE * u];
                 lvn[u] = lv_s[buf][jn][col + WAVE * u];
             }
+            // latency maximum over the candidates (a non-candidate, NaN base
+            // score, contributes 0)
             float T[IPL];
-            float tmax = -INFINITY;
+            uint32_t tb = 0;
 #pragma unroll
             for (int u = 0; u < IPL; ++u) {
                 T[u] = latency(p[u], a[u], rP[u], rD[u], l, lv[u]);
-                if (bs[u] == bs[u])   // a candidate
-                    tmax = fmaxf(tmax, T[u]);
+                tb = umax(tb, bs[u] == bs[u] ? __float_as_uint(T[u]) : 0u);
             }
-            tmax = fmax_all(tmax);
-            uint32_t best = 0;   // f2key of this lane's best score (0 = no candidate)
-            int bu = 0;
+            const float tmax = __uint_as_float(umax_all(tb));
+            // keys of S * Tmax; 0 for a non-candidate
+            uint32_t key[IPL], kb = 0;
 #pragma unroll
             for (int u = 0; u < IPL; ++u) {
-                const float S = full_score(bs[u], T[u], tmax, wl);
-                const uint32_t key = f2key(S);
-                if (S == S && key > best) {   // slots ascend in index: ties keep the lower
-                    best = key;
-                    bu = u;
+                const float v = fmaf(bs[u], tmax, wl * (tmax - T[u]));
+                key[u] = bs[u] == bs[u] ? __float_as_uint(v) + 1u : 0u;
+                kb = umax(kb, key[u]);
+            }
+            const uint32_t kmax = umax_all(kb);
+            // lowest instance holding the maximum (slots ascend in index)
+            int istar = -1, ustar = 0;
+            if (kmax != 0) {
+#pragma unroll
+                for (int u = 0; u < IPL; ++u) {
+                    uint64_t mk = ballot(key[u] == kmax);
+                    if (WIDTH == 16)
+                        mk &= 0xffffull;   // the four rows hold the same instances
+                    if (istar < 0 && mk != 0) {
+                        istar = WAVE * u + (int)__builtin_ctzll(mk);
+                        ustar = u;
+                    }
                 }
             }
-            uint32_t hi = best, lo = best ? ~(uint32_t)inst(bu) : 0u;
-            reduce_max_pair<WIDTH>(hi, lo);
-            const bool found = hi != 0;
-            const int istar = found ? (int)~lo : -1;
-            if (lane == 0) {
-                assign[r] = istar;
-                if (chosen)
-                    chosen[r] = found ? key2f(hi) : __builtin_nanf("");
+            // capture the pick: its base score and latency from the lane
+            // and slot holding it
+            const int slot = j & (WAVE - 1);
+            if (chosen && istar >= 0) {
+                float vb = bs[0], vt = T[0];
+#pragma unroll
+                for (int u = 1; u < IPL; ++u) {
+                    vb = ustar == u ? bs[u] : vb;
+                    vt = ustar == u ? T[u] : vt;
+                }
+                const int src = istar & (WAVE - 1);
+                vb = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, vb), src));
+                vt = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, vt), src));
+                if (lane == slot) {
+                    cap_b = vb;
+                    cap_t = vt;
+                }
+            }
+            if (lane == slot) {
+                cap_i = istar;
+                cap_r = r;
+                cap_m = tmax;
+            }
+            // write the captured steps: every 64 steps and at the chunk's end
+            if (slot == WAVE - 1 || j == rows - 1) {
+                if (lane <= slot) {
+                    assign[cap_r] = cap_i;
+                    if (chosen)
+                        chosen[cap_r] = cap_i >= 0 ? full_score(cap_b, cap_t, cap_m, wl)
+                                                   : __builtin_nanf("");
+                }
             }
 #pragma unroll
             for (int u = 0; u < IPL; ++u) {
-                if (found && inst(u) == istar) {
+                if (inst(u) == istar) {
                     p[u] += l;
                     a[u] += lv[u];
                 }
@@ -351,8 +409,8 @@ hipError_t launch_assign(const float *q_hat, const float *l_hat, const int32_t *
 {
     const int ipl = (I + WAVE - 1) / WAVE;
 #define RB_ASSIGN(N, W)                                                                          \
-    hipLaunchKernelGGL((assign_kernel<N, W>), dim3(1), dim3(ASSIGN_THREADS), 0, s, q_hat, l_hat, \
-                       plen, B, M, in, I, wq, wl, wc, opt, assign, chosen)
+    hipLaunchKernelGGL((assign_kernel<N, W>), dim3(1), dim3(assign_threads<N>()), 0, s, q_hat,   \
+                       l_hat, plen, B, M, in, I, wq, wl, wc, opt, assign, chosen)
     if (I <= 16) RB_ASSIGN(1, 16);
     else if (ipl <= 1) RB_ASSIGN(1, 64);
     else if (ipl <= 2) RB_ASSIGN(2, 64);
