@@ -14,8 +14,13 @@ namespace rb {
 constexpr int SCAN_THREADS = 512;   // 8 waves, two per SIMD
 constexpr int SCAN_WAVES = 8;
 constexpr int SCAN_RT = 2;          // 16-row MFMA tiles per wave per iteration (32 rows)
-constexpr int SCAN_PREFETCH = 1;    // k-steps whose loads are in flight ahead of the MFMAs
-constexpr int SCAN_UNROLL = 2;      // register ring of bank fragments; k-steps are padded to it
+constexpr int SCAN_KPAD = 4;        // k-steps per row are padded to a multiple of this
+// Register ring of bank fragments (k-steps; the loop is unrolled by it), with
+// its size less one k-step of loads in flight ahead of the MFMAs: 2 for a
+// full 256-query tile, whose 128 accumulators leave room for no more, 4 for
+// smaller tiles, which do less work per k-step and need the deeper prefetch.
+template <int NG>
+constexpr int scan_ring() { return NG >= 16 ? 2 : 4; }
 constexpr int STAGE_CAP = 128;      // per-wave LDS staging of one iteration's candidates
 constexpr size_t LDS_LIMIT = 160 * 1024;
 constexpr int MERGE_WAVES = 4;      // queries per merge workgroup, one wave each
@@ -38,7 +43,7 @@ constexpr int SEED_MAX_GROUPS = 2048;  // S / 16 for S <= 32768
 struct KnnPlan {
     int dtype;          // 0 fp32, 1 bf16
     int B, N, d, k;
-    int nks, nksp;      // 64-byte k-steps per row, padded to SCAN_UNROLL
+    int nks, nksp;      // 64-byte k-steps per row, padded to SCAN_KPAD
     int ng, gr, rt;     // query groups of 16 per tile (gr of them resident), 16-row tiles per wave
     int n_qt, n_chunks, W;
     long rows_per_chunk;

@@ -473,7 +473,7 @@ int plan_knn(int B, int N, int d, int dtype, int k, int num_cu, KnnPlan *p, int 
     p->d = d;
     p->k = k;
     p->nks = (d + 4 * vec - 1) / (4 * vec);
-    p->nksp = (p->nks + SCAN_UNROLL - 1) / SCAN_UNROLL * SCAN_UNROLL;
+    p->nksp = (p->nks + SCAN_KPAD - 1) / SCAN_KPAD * SCAN_KPAD;
     // largest query tile that B can fill and whose lists fit in LDS; then as
     // many of its query groups resident in LDS as the rest of the space holds
     int want = 1;

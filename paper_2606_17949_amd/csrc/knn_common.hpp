@@ -24,7 +24,7 @@ struct ScanArgs {
 // Byte offsets of the scan's LDS regions for a tile of ng query groups of
 // which the first gr are resident for the whole kernel.
 struct ScanLayout {
-    uint32_t res, strm, list, qn, gb, lmk, nx, sq, sk, si, bytes;
+    uint32_t res, strm, list, qn, gb, lmk, nu, nx, sq, sk, si, bytes;
 };
 
 __host__ __device__ inline ScanLayout scan_layout(int ng, int gr, int nksp, int k, int rt)
@@ -43,6 +43,8 @@ __host__ __device__ inline ScanLayout scan_layout(int ng, int gr, int nksp, int 
     L.gb = o;      // [bm] snapshot of the shared bound
     o += bm * 4;
     L.lmk = o;     // [bm] an upper bound of each list's largest key
+    o += bm * 4;
+    L.nu = o;      // [bm] each query's candidate threshold on the accumulators
     o += bm * 4;
     L.nx = o;      // [waves][2][16*rt] -|x|^2/2 of this and the next iteration's rows
     o += SCAN_WAVES * 2 * rt * 16 * 4;

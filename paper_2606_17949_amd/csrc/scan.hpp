@@ -43,7 +43,8 @@ __global__ __launch_bounds__(SCAN_THREADS, 1) void scan_kernel(const ScanArgs A)
     constexpr int RW = RT * 16;                    // rows per wave per iteration
     constexpr int RWG = SCAN_WAVES * RW;           // rows per workgroup iteration
     constexpr int QPT = (NS * WAVE + SCAN_THREADS - 1) / SCAN_THREADS;   // stream items per thread
-    constexpr int R = SCAN_UNROLL, P = SCAN_PREFETCH, QS = 2;
+    constexpr int R = scan_ring<NG>(), P = R - 1, QS = 2;
+    static_assert(SCAN_KPAD % R == 0, "padded k-steps fill whole ring cycles");
     constexpr int NB = NG < 4 ? NG : 4;            // query fragments in flight
     static_assert(P < R, "prefetch distance must leave a free ring slot");
     static_assert(R % QS == 0 && R % 2 == 0, "staging slots and LDS buffers divide the unroll");
@@ -58,6 +59,7 @@ __global__ __launch_bounds__(SCAN_THREADS, 1) void scan_kernel(const ScanArgs A)
     float *qn_s = (float *)(smem + L.qn);
     uint32_t *gb_s = (uint32_t *)(smem + L.gb);
     uint32_t *lmk_s = (uint32_t *)(smem + L.lmk);
+    uint32_t *nu_s = (uint32_t *)(smem + L.nu);   // float bits
 
     // Workgroup -> (chunk c, query tile t). Workgroups are dispatched to the
     // eight XCDs round robin, so this map puts every query tile of one chunk
@@ -266,6 +268,14 @@ __global__ __launch_bounds__(SCAN_THREADS, 1) void scan_kernel(const ScanArgs A)
         }
     };
 
+    // each query's threshold, recomputed after every iteration's inserts and
+    // bound refresh (a value from before a later lowering of the bound is
+    // smaller, so it only lets more candidates through)
+    auto refresh_nu = [&](int i) { lds_store_relaxed(nu_s + i, __float_as_uint(nu_of(i))); };
+    for (int i = tid; i < BM; i += SCAN_THREADS)
+        refresh_nu(i);
+    auto nu_read = [&](int i) -> float { return __uint_as_float(lds_load_relaxed(nu_s + i)); };
+
     // ---- pipeline prologue
 #pragma unroll
     for (int u = 0; u < P; ++u)
@@ -313,7 +323,7 @@ __global__ __launch_bounds__(SCAN_THREADS, 1) void scan_kernel(const ScanArgs A)
         static_for<0, NG / TB>([&](auto GB) {
             constexpr int g0 = decltype(GB)::value * TB;
             float nus[TB];
-            static_for<0, TB>([&](auto G) { nus[G.value] = nu_of((g0 + G.value) * 16 + col); });
+            static_for<0, TB>([&](auto G) { nus[G.value] = nu_read((g0 + G.value) * 16 + col); });
             static_for<0, TB>([&](auto G) {
                 constexpr int g = g0 + decltype(G)::value;
                 float m = -INFINITY;
@@ -330,7 +340,7 @@ __global__ __launch_bounds__(SCAN_THREADS, 1) void scan_kernel(const ScanArgs A)
             if (!(hits >> g & 1u))
                 return;
             const int i = g * 16 + col;
-            const float nu = nu_of(i);
+            const float nu = nu_read(i);
             const float qq = qn_s[i];
             static_for<0, RT>([&](auto TT) {
                 constexpr int tt = decltype(TT)::value;
@@ -376,10 +386,12 @@ __global__ __launch_bounds__(SCAN_THREADS, 1) void scan_kernel(const ScanArgs A)
             insert_lanes(s < nst, vi, vk, vx);
         }
         // pick up bounds other workgroups have lowered
-        for (int i = tid; i < BM; i += SCAN_THREADS)
+        for (int i = tid; i < BM; i += SCAN_THREADS) {
             if (q0 + i < A.B)
                 lds_store_relaxed(gb_s + i, __hip_atomic_load(A.tau + q0 + i, __ATOMIC_RELAXED,
                                                               __HIP_MEMORY_SCOPE_AGENT));
+            refresh_nu(i);
+        }
     }
 
     // ---- the workgroup's lists -> workspace [B][n_chunks][k], valid entries first
