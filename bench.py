@@ -91,7 +91,49 @@ def parse():
                          "PMC_DIR/copywrite) into PMC_DIR/scan_traffic.json for --workload")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain device copy of 1 GiB (counter calibration)")
+    ap.add_argument("--ceilings", action="store_true",
+                    help="only measure the practical ceilings: a read-only pass over 4 GiB and "
+                         "a library bf16 GEMM of the largebatch shape (yardsticks, not the path)")
+    ap.add_argument("--cold", action="store_true",
+                    help="time each batch alone (sequential) after writing a 512 MiB buffer, so "
+                         "that the bank is not resident in the last-level cache; prints the "
+                         "per-batch median and p10/p90")
     return ap.parse_args()
+
+
+def ceilings():
+    """Practical ceilings on this device, as yardsticks for the roofline
+    fractions: a read-only reduction over 4 GiB (torch) and a bf16 GEMM of the
+    largebatch shape, 1,000,000 x 1,024 by 1,024 x 1,024 (torch / hipBLASLt)."""
+    import torch
+    dev = torch.device("cuda:0")
+    out = {}
+    x = torch.ones(1 << 31, dtype=torch.bfloat16, device=dev)      # 4 GiB
+    for _ in range(2):
+        x.sum(dtype=torch.float32)
+    torch.cuda.synchronize()
+    b, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    b.record()
+    for _ in range(5):
+        x.sum(dtype=torch.float32)
+    e.record()
+    torch.cuda.synchronize()
+    out["read_probe_gbps"] = round(x.numel() * 2 * 5 / (b.elapsed_time(e) / 1e3) / 1e9, 1)
+    del x
+    bank = torch.randn(1_000_000, 1024, device=dev).to(torch.bfloat16)
+    q = torch.randn(1024, 1024, device=dev).to(torch.bfloat16)
+    for _ in range(2):
+        torch.mm(bank, q)
+    torch.cuda.synchronize()
+    b.record()
+    for _ in range(5):
+        torch.mm(bank, q)
+    e.record()
+    torch.cuda.synchronize()
+    flops = 2.0 * 1_000_000 * 1024 * 1024
+    out["gemm_bf16_tflops"] = round(flops * 5 / (b.elapsed_time(e) / 1e3) / 1e12, 1)
+    out["gemm_shape"] = "1,000,000 x 1,024 @ 1,024 x 1,024 bf16 (fp32 accumulate)"
+    print(json.dumps(out), flush=True)
 
 
 def calibrate_copy():
@@ -150,6 +192,9 @@ def main():
         sys.exit(2)
     if args.calibrate_copy:
         calibrate_copy()
+        return
+    if args.ceilings:
+        ceilings()
         return
 
     import numpy as np
@@ -267,6 +312,31 @@ def main():
     run(list(range(W)))
     torch.cuda.synchronize()
     log("warm-up done")
+
+    if args.cold:
+        # each batch alone, after a 512 MiB write that evicts the bank from
+        # the last-level cache (untimed); sequential fused calls
+        flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+        times = []
+        for j in range(K):
+            flush.fill_(j & 255)
+            torch.cuda.synchronize()
+            b0, b1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            b0.record(stream)
+            step(W + j)
+            b1.record(stream)
+            torch.cuda.synchronize()
+            times.append(b0.elapsed_time(b1))
+        med = float(np.median(times))
+        print(json.dumps({"metric": "routing decisions/sec, cold bank (per batch, median)",
+                          "value": round(cfg.B / (med / 1e3), 1), "unit": "decisions/s",
+                          "workload": cfg.name, "batches": K,
+                          "ms_per_batch": {"median": round(med, 4),
+                                           "p10": round(float(np.percentile(times, 10)), 4),
+                                           "p90": round(float(np.percentile(times, 90)), 4)},
+                          "bank_gbps_at_median": round(cfg.bank_bytes() / (med / 1e3) / 1e9, 1)}),
+              flush=True)
+        return
 
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
