@@ -252,109 +252,112 @@ __global__ __launch_bounds__(assign_threads<IPL>()) void assign_kernel(
         else
             return wave_reduce(v, umax);
     };
-    // captured picks, step (j mod 64) in lane (j mod 64)
-    int cap_i = -1, cap_r = 0;
+    // Steps go in blocks of 64: lane s holds step (block + s)'s request index
+    // and prompt length, read from LDS once per block (a step takes its
+    // prompt length with a lane read, not an LDS round trip), and captures
+    // that step's pick.
+    int cap_i = -1;
     float cap_b = 0.f, cap_t = 0.f, cap_m = 0.f;
     __syncthreads();   // chunk 0 is ready
     for (int c = 0; c < n_ch; ++c) {
         const int buf = c & 1;
         const int rows = min(CH, B - c * CH);
-        float l = l_s[buf][0], bs[IPL], lv[IPL];
-        int r = r_s[buf][0];
+        float bs[IPL], lv[IPL];
 #pragma unroll
         for (int u = 0; u < IPL; ++u) {
             bs[u] = base_s[buf][0][col + WAVE * u];
             lv[u] = lv_s[buf][0][col + WAVE * u];
         }
-        for (int j = 0; j < rows; ++j) {
-            // next step's values, in flight while this one is decided
-            const int jn = j + 1 < rows ? j + 1 : j;
-            const float ln = l_s[buf][jn];
-            const int rn = r_s[buf][jn];
-            float bsn[IPL], lvn[IPL];
-#pragma unroll
-            for (int u = 0; u < IPL; ++u) {
-                bsn[u] = base_s[buf][jn][col + WAVE * u];
-                lvn[u] = lv_s[buf][jn][col + WAVE * u];
-            }
-            // latency maximum over the candidates (a non-candidate, NaN base
-            // score, contributes 0)
-            float T[IPL];
-            uint32_t tb = 0;
-#pragma unroll
-            for (int u = 0; u < IPL; ++u) {
-                T[u] = latency(p[u], a[u], rP[u], rD[u], l, lv[u]);
-                tb = umax(tb, bs[u] == bs[u] ? __float_as_uint(T[u]) : 0u);
-            }
-            const float tmax = __uint_as_float(umax_all(tb));
-            // keys of S * Tmax; 0 for a non-candidate
-            uint32_t key[IPL], kb = 0;
-#pragma unroll
-            for (int u = 0; u < IPL; ++u) {
-                const float v = fmaf(bs[u], tmax, wl * (tmax - T[u]));
-                key[u] = bs[u] == bs[u] ? __float_as_uint(v) + 1u : 0u;
-                kb = umax(kb, key[u]);
-            }
-            const uint32_t kmax = umax_all(kb);
-            // lowest instance holding the maximum (slots ascend in index)
-            int istar = -1, ustar = 0;
-            if (kmax != 0) {
+        for (int jb = 0; jb < rows; jb += WAVE) {
+            const int nb = min(WAVE, rows - jb);   // steps of this block
+            const int jj = jb + min(lane, nb - 1);
+            const int rblk = r_s[buf][jj];
+            const float lblk = l_s[buf][jj];
+            for (int slot = 0; slot < nb; ++slot) {
+                const int j = jb + slot;
+                const float l = __builtin_bit_cast(
+                    float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, lblk), slot));
+                // next step's values, in flight while this one is decided
+                const int jn = j + 1 < rows ? j + 1 : j;
+                float bsn[IPL], lvn[IPL];
 #pragma unroll
                 for (int u = 0; u < IPL; ++u) {
-                    uint64_t mk = ballot(key[u] == kmax);
-                    if (WIDTH == 16)
-                        mk &= 0xffffull;   // the four rows hold the same instances
-                    if (istar < 0 && mk != 0) {
-                        istar = WAVE * u + (int)__builtin_ctzll(mk);
-                        ustar = u;
+                    bsn[u] = base_s[buf][jn][col + WAVE * u];
+                    lvn[u] = lv_s[buf][jn][col + WAVE * u];
+                }
+                // latency maximum over the candidates (a non-candidate, NaN
+                // base score, contributes 0)
+                float T[IPL];
+                uint32_t tb = 0;
+#pragma unroll
+                for (int u = 0; u < IPL; ++u) {
+                    T[u] = latency(p[u], a[u], rP[u], rD[u], l, lv[u]);
+                    tb = umax(tb, bs[u] == bs[u] ? __float_as_uint(T[u]) : 0u);
+                }
+                const float tmax = __uint_as_float(umax_all(tb));
+                // keys of S * Tmax; 0 for a non-candidate
+                uint32_t key[IPL], kb = 0;
+#pragma unroll
+                for (int u = 0; u < IPL; ++u) {
+                    const float v = fmaf(bs[u], tmax, wl * (tmax - T[u]));
+                    key[u] = bs[u] == bs[u] ? __float_as_uint(v) + 1u : 0u;
+                    kb = umax(kb, key[u]);
+                }
+                const uint32_t kmax = umax_all(kb);
+                // lowest instance holding the maximum (slots ascend in index)
+                int istar = -1, ustar = 0;
+                if (kmax != 0) {
+#pragma unroll
+                    for (int u = 0; u < IPL; ++u) {
+                        uint64_t mk = ballot(key[u] == kmax);
+                        if (WIDTH == 16)
+                            mk &= 0xffffull;   // the four rows hold the same instances
+                        if (istar < 0 && mk != 0) {
+                            istar = WAVE * u + (int)__builtin_ctzll(mk);
+                            ustar = u;
+                        }
                     }
                 }
-            }
-            // capture the pick: its base score and latency from the lane
-            // and slot holding it
-            const int slot = j & (WAVE - 1);
-            if (chosen && istar >= 0) {
-                float vb = bs[0], vt = T[0];
+                // capture the pick in lane `slot`: the instance, Tmax and, for
+                // the scores, the pick's base score and latency from the lane
+                // and slot holding it
+                const bool mine = lane == slot;
+                cap_i = mine ? istar : cap_i;
+                cap_m = mine ? tmax : cap_m;
+                if (chosen && istar >= 0) {
+                    float vb = bs[0], vt = T[0];
 #pragma unroll
-                for (int u = 1; u < IPL; ++u) {
-                    vb = ustar == u ? bs[u] : vb;
-                    vt = ustar == u ? T[u] : vt;
+                    for (int u = 1; u < IPL; ++u) {
+                        vb = ustar == u ? bs[u] : vb;
+                        vt = ustar == u ? T[u] : vt;
+                    }
+                    const int src = istar & (WAVE - 1);
+                    vb = __builtin_bit_cast(
+                        float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, vb), src));
+                    vt = __builtin_bit_cast(
+                        float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, vt), src));
+                    cap_b = mine ? vb : cap_b;
+                    cap_t = mine ? vt : cap_t;
                 }
-                const int src = istar & (WAVE - 1);
-                vb = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, vb), src));
-                vt = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, vt), src));
-                if (lane == slot) {
-                    cap_b = vb;
-                    cap_t = vt;
-                }
-            }
-            if (lane == slot) {
-                cap_i = istar;
-                cap_r = r;
-                cap_m = tmax;
-            }
-            // write the captured steps: every 64 steps and at the chunk's end
-            if (slot == WAVE - 1 || j == rows - 1) {
-                if (lane <= slot) {
-                    assign[cap_r] = cap_i;
-                    if (chosen)
-                        chosen[cap_r] = cap_i >= 0 ? full_score(cap_b, cap_t, cap_m, wl)
-                                                   : __builtin_nanf("");
-                }
-            }
 #pragma unroll
-            for (int u = 0; u < IPL; ++u) {
-                if (inst(u) == istar) {
-                    p[u] += l;
-                    a[u] += lv[u];
+                for (int u = 0; u < IPL; ++u) {
+                    if (inst(u) == istar) {
+                        p[u] += l;
+                        a[u] += lv[u];
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < IPL; ++u) {
+                    bs[u] = bsn[u];
+                    lv[u] = lvn[u];
                 }
             }
-            l = ln;
-            r = rn;
-#pragma unroll
-            for (int u = 0; u < IPL; ++u) {
-                bs[u] = bsn[u];
-                lv[u] = lvn[u];
+            // write the block's picks and their Eq. 1 scores in one pass
+            if (lane < nb) {
+                assign[rblk] = cap_i;
+                if (chosen)
+                    chosen[rblk] = cap_i >= 0 ? full_score(cap_b, cap_t, cap_m, wl)
+                                              : __builtin_nanf("");
             }
         }
         __syncthreads();   // buffer c & 1 may now be refilled; chunk c + 1 is ready
