@@ -37,7 +37,8 @@ FP32_PEAK_TFLOPS = 157.3
 
 # Sources the scan kernel is built from: measured traffic is reported only for
 # the build whose sources it was taken with.
-SCAN_SOURCES = ["paper_2606_17949_amd/csrc/scan.hpp", "paper_2606_17949_amd/csrc/knn_common.hpp",
+SCAN_SOURCES = ["paper_2606_17949_amd/csrc/scan.hpp", "paper_2606_17949_amd/csrc/scan_rq.hpp",
+                "paper_2606_17949_amd/csrc/knn_common.hpp",
                 "paper_2606_17949_amd/csrc/kernels.hpp", "paper_2606_17949_amd/csrc/common.hpp"]
 TRAFFIC_FILE = "profiles/scan_traffic.json"
 
@@ -370,7 +371,8 @@ def main():
         tf = flops / (scan_avg / 1e3) / 1e12
         roof = {"bound": "mfma", "achieved": round(tf, 1), "peak": peak_tf, "unit": "TFLOP/s",
                 "frac": round(tf / peak_tf, 4), "traffic": measured_traffic(cfg.name)}
-    roof["kernel"] = "scan_kernel (bank distance contraction + fused per-chunk top-k)"
+    roof["kernel"] = ("bank scan, scan_kernel or rq_scan_kernel (distance contraction + fused "
+                      "per-chunk top-k)")
     roof["per_launch"] = {"bytes": bank_bytes, "flops": flops, "avg_us": round(scan_avg * 1e3, 2),
                           "p10_us": round(float(np.percentile(scan_ms, 10)) * 1e3, 2),
                           "p90_us": round(float(np.percentile(scan_ms, 90)) * 1e3, 2)}

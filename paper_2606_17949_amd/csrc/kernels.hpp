@@ -15,12 +15,18 @@ constexpr int SCAN_THREADS = 512;   // 8 waves, two per SIMD
 constexpr int SCAN_WAVES = 8;
 constexpr int SCAN_RT = 2;          // 16-row MFMA tiles per wave per iteration (32 rows)
 constexpr int SCAN_KPAD = 4;        // k-steps per row are padded to a multiple of this
-// Register ring of bank fragments (k-steps; the loop is unrolled by it), with
-// its size less one k-step of loads in flight ahead of the MFMAs: 2 for a
-// full 256-query tile, whose 128 accumulators leave room for no more, 4 for
-// smaller tiles, which do less work per k-step and need the deeper prefetch.
-template <int NG>
-constexpr int scan_ring() { return NG >= 16 ? 2 : 4; }
+// Ring depth of the scan's loads, in k-steps (the loop is unrolled by it):
+// bank fragments go to a register ring and streamed query fragments to an LDS
+// ring of as many slots, both depth - 1 k-steps ahead of the MFMAs. Four for
+// tiles below 256 queries. For a full tile, four only for bf16 rows of whole
+// k-steps with less than half the tile resident (the fp32 MFMA steps and the
+// lane masks of a partial k-step take the registers, and with half the tile
+// resident or more the LDS serves better as resident queries than as ring
+// slots).
+__host__ __device__ constexpr int scan_ring(int dtype, int ng, int gr, bool ragged)
+{
+    return ng < 16 || (dtype == 1 && !ragged && gr < ng / 2) ? 4 : 2;
+}
 constexpr int STAGE_CAP = 128;      // per-wave LDS staging of one iteration's candidates
 constexpr size_t LDS_LIMIT = 160 * 1024;
 constexpr int MERGE_WAVES = 4;      // queries per merge workgroup, one wave each
@@ -28,8 +34,20 @@ constexpr int MERGE_CAP = 2048;     // candidates per query the merge holds in L
 constexpr int MERGE_MAX_LISTS = 64 * 64;   // 64 lists per lane
 constexpr int RB_MAX_K_DEV = 64;    // largest k (the ABI limit)
 constexpr int SEED_MAX_GROUPS = 2048;  // S / 16 for S <= 32768
+// The query-resident scan (a batch of at most RQ_WAVES*RQ_QW*16 queries of
+// RQ_NKS full k-steps, k <= RQ_MAX_K): RQ_WAVES waves of RQ_QW query groups,
+// blocks of RQ_ROWS bank rows, stages of RQ_KSTG k-steps of a block, a ring
+// of RQ_STAGES stages in LDS.
+constexpr int RQ_WAVES = 8;
+constexpr int RQ_QW = 2;
+constexpr int RQ_ROWS = 32;
+constexpr int RQ_KSTG = 8;
+constexpr int RQ_STAGES = 7;
+constexpr int RQ_NKS = 24;
+constexpr int RQ_MAX_K = 16;
 
-// How one rb_knn_topk call is split.
+// How one rb_knn_topk call is split (the tile scan; the query-resident scan
+// differs in that one workgroup holds the whole batch, so n_qt = 1).
 //  * seed: S bank rows spread evenly over the bank; per query, the k-th
 //    smallest of the S/16 minima over groups of 16 of them bounds the k-th
 //    nearest distance from above (k distinct rows lie at or below it).
@@ -41,6 +59,8 @@ constexpr int SEED_MAX_GROUPS = 2048;  // S / 16 for S <= 32768
 //    candidates that pass the bound.
 //  * merge: per query, the k smallest of its W = n_chunks lists.
 struct KnnPlan {
+    int kind;           // 0 tile scan, 1 query-resident scan
+    int qw;             // query groups per wave of the query-resident scan
     int dtype;          // 0 fp32, 1 bf16
     int B, N, d, k;
     int nks, nksp;      // 64-byte k-steps per row, padded to SCAN_KPAD

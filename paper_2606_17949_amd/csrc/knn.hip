@@ -474,34 +474,52 @@ int plan_knn(int B, int N, int d, int dtype, int k, int num_cu, KnnPlan *p, int 
     p->k = k;
     p->nks = (d + 4 * vec - 1) / (4 * vec);
     p->nksp = (p->nks + SCAN_KPAD - 1) / SCAN_KPAD * SCAN_KPAD;
-    // largest query tile that B can fill and whose lists fit in LDS; then as
-    // many of its query groups resident in LDS as the rest of the space holds
+    const bool ragged = d % (4 * vec) != 0;
+    // a batch of 65..256 queries of bf16 rows of RQ_NKS full k-steps stays in
+    // the registers of one workgroup; smaller batches fit the tile scan's LDS
+    // whole
+    p->kind = dtype == 1 && !ragged && p->nks == RQ_NKS && B > 64 &&
+                      B <= RQ_WAVES * RQ_QW * 16 && k <= RQ_MAX_K
+                  ? 1
+                  : 0;
+    p->qw = p->kind == 1 ? RQ_QW : 0;
+    // tile scan: largest query tile that B can fill and whose lists fit in
+    // LDS; then as many of its query groups resident in LDS as the rest of
+    // the space holds
     int want = 1;
     while (want < 16 && want * 16 < B)
         want *= 2;
     p->ng = 0;
     for (int ng = want; ng >= 1; ng /= 2) {
-        if (scan_layout(ng, 0, p->nksp, k, SCAN_RT).bytes <= LDS_LIMIT) {
+        const int slots = scan_ring(dtype, ng, 0, ragged);
+        if (scan_layout(ng, 0, p->nksp, k, SCAN_RT, slots).bytes <= LDS_LIMIT) {
             p->ng = ng;
             break;
         }
     }
     if (p->ng == 0)
         return -1;
-    // resident query groups: all, half, a quarter or none of the tile (the
-    // counts the scan is compiled for), the most that fit
-    const int gr_opts[4] = {p->ng, p->ng / 2, p->ng / 4, 0};
+    // resident query groups: all, half, a quarter, an eighth or none of the
+    // tile (the counts the scan is compiled for), the most that fit
+    const int gr_opts[5] = {p->ng, p->ng / 2, p->ng / 4, p->ng / 8, 0};
     p->gr = 0;
     for (int gr : gr_opts) {
-        if (scan_layout(p->ng, gr, p->nksp, k, SCAN_RT).bytes <= LDS_LIMIT) {
+        const int slots = scan_ring(dtype, p->ng, gr, ragged);
+        if (scan_layout(p->ng, gr, p->nksp, k, SCAN_RT, slots).bytes <= LDS_LIMIT) {
             p->gr = gr;
             break;
         }
     }
-    p->lds_bytes = scan_layout(p->ng, p->gr, p->nksp, k, SCAN_RT).bytes;
+    p->lds_bytes = scan_layout(p->ng, p->gr, p->nksp, k, SCAN_RT,
+                               scan_ring(dtype, p->ng, p->gr, ragged))
+                       .bytes;
     p->rt = SCAN_RT;
     const int bm = p->ng * 16;
     p->n_qt = B > 0 ? (B + bm - 1) / bm : 1;
+    if (p->kind == 1) {
+        p->n_qt = 1;
+        p->lds_bytes = rq_layout(k, p->qw).bytes;
+    }
     // one workgroup per compute unit (the LDS use allows no more); with
     // `reserve`, that many units of each XCD stay free: workgroups go to the
     // XCDs round robin and the tiles of a chunk share its XCD, so a whole
@@ -561,8 +579,8 @@ int plan_knn(int B, int N, int d, int dtype, int k, int num_cu, KnnPlan *p, int 
     // candidate overflow: per scan wave, every (row, query) pair of one
     // iteration beyond the LDS staging area
     const long pairs = (long)SCAN_RT * 16 * p->ng * 16;
-    p->ovf_cap = pairs > STAGE_CAP ? (int)(pairs - STAGE_CAP) : 0;
-    p->grid = ((p->n_chunks + 7) / 8) * 8 * p->n_qt;
+    p->ovf_cap = p->kind == 0 && pairs > STAGE_CAP ? (int)(pairs - STAGE_CAP) : 0;
+    p->grid = p->kind == 1 ? p->n_chunks : ((p->n_chunks + 7) / 8) * 8 * p->n_qt;
     p->off_ovf = off;
     off += align256((size_t)p->grid * SCAN_WAVES * 3 * (p->ovf_cap > 0 ? p->ovf_cap : 1) * 4);
     p->bytes = off;
@@ -659,8 +677,11 @@ hipError_t launch_knn(const KnnPlan &p, const void *queries, const void *bank,
     if (timed && (e = hipEventRecord(t_scan_begin, s)) != hipSuccess)
         return e;
     const bool ragged = p.d % (p.dtype == 1 ? 32 : 16) != 0;
-    e = p.dtype == 1 ? (ragged ? launch_scan_bf16_ragged(p, a, s) : launch_scan_bf16(p, a, s))
-                     : (ragged ? launch_scan_f32_ragged(p, a, s) : launch_scan_f32(p, a, s));
+    if (p.kind == 1)
+        e = launch_scan_rq(p, a, s);
+    else
+        e = p.dtype == 1 ? (ragged ? launch_scan_bf16_ragged(p, a, s) : launch_scan_bf16(p, a, s))
+                         : (ragged ? launch_scan_f32_ragged(p, a, s) : launch_scan_f32(p, a, s));
     if (e != hipSuccess)
         return e;
     if (timed && (e = hipEventRecord(t_scan_end, s)) != hipSuccess)

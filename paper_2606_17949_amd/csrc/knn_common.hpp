@@ -22,20 +22,22 @@ struct ScanArgs {
 };
 
 // Byte offsets of the scan's LDS regions for a tile of ng query groups of
-// which the first gr are resident for the whole kernel.
+// which the first gr are resident for the whole kernel, with a ring of
+// `slots` k-steps for the others.
 struct ScanLayout {
     uint32_t res, strm, list, qn, gb, lmk, nu, nx, sq, sk, si, bytes;
 };
 
-__host__ __device__ inline ScanLayout scan_layout(int ng, int gr, int nksp, int k, int rt)
+__host__ __device__ inline ScanLayout scan_layout(int ng, int gr, int nksp, int k, int rt, int slots)
 {
     ScanLayout L;
     const uint32_t bm = (uint32_t)ng * 16, frag = WAVE * 16;
     uint32_t o = 0;
     L.res = o;     // [nksp][gr][64] fragments of the resident groups, every k-step
     o += (uint32_t)nksp * gr * frag;
-    L.strm = o;    // [2][ng - gr][64] fragments of the other groups for one k-step
-    o += 2u * (ng - gr) * frag;
+    L.strm = o;    // [slots][ng - gr][64] fragments of the other groups, one k-step per
+    // slot, and a sink fragment for loads with no destination
+    o += gr < ng ? (uint32_t)(slots * (ng - gr) + 1) * frag : 0u;
     L.list = o;    // [bm][k] (key << 32 | index), the workgroup's candidate lists
     o += bm * k * 8;
     L.qn = o;      // [bm] |q|^2
@@ -58,8 +60,31 @@ __host__ __device__ inline ScanLayout scan_layout(int ng, int gr, int nksp, int 
     return L;
 }
 
+// Byte offsets of the query-resident scan's LDS regions.
+struct RqLayout {
+    uint32_t ring, norms, lists, qinfo, bytes;
+};
+
+__host__ __device__ inline RqLayout rq_layout(int k, int qw)
+{
+    RqLayout L;
+    uint32_t o = 0;
+    L.ring = o;    // [RQ_STAGES][RQ_KSTG * RQ_ROWS / 16][64] bank fragments
+    o += (uint32_t)RQ_STAGES * RQ_KSTG * (RQ_ROWS / 16) * WAVE * 16;
+    L.norms = o;   // [RQ_STAGES][64] |x|^2 of the rows of a block (with its first stage)
+    o += (uint32_t)RQ_STAGES * WAVE * 4;
+    L.lists = o;   // [waves][16 * qw][k] (key << 32 | index), one list per owned query
+    o += (uint32_t)RQ_WAVES * qw * 16 * k * 8;
+    L.qinfo = o;   // [waves][16 * qw] |q|^2, then [waves][16 * qw] the shared bound
+    o += (uint32_t)RQ_WAVES * qw * 16 * 8;
+    L.bytes = o;
+    return L;
+}
+
 // The bank-scan launchers, one translation unit per element type and
-// k-step raggedness (they are the bulk of the compile time).
+// k-step raggedness (they are the bulk of the compile time), and one for the
+// query-resident scan.
+hipError_t launch_scan_rq(const KnnPlan &p, const ScanArgs &a, hipStream_t s);
 hipError_t launch_scan_bf16(const KnnPlan &p, const ScanArgs &a, hipStream_t s);
 hipError_t launch_scan_bf16_ragged(const KnnPlan &p, const ScanArgs &a, hipStream_t s);
 hipError_t launch_scan_f32(const KnnPlan &p, const ScanArgs &a, hipStream_t s);
@@ -133,6 +158,25 @@ __device__ __forceinline__ i32x4 buffer_load16(__amdgpu_buffer_rsrc_t r, uint32_
 
 constexpr uint32_t OFF_NONE = 0x80000000u;   // a buffer offset past any resource
 
+// Global -> LDS load of 16 bytes per lane through the buffer resource: lane l's
+// bytes land at dst + 16*l (dst is the same for the whole wave); a lane whose
+// offset falls outside the resource writes zeros. Completion is counted by
+// the wave's vector memory counter, like a load into registers.
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, i32x4 *dst, uint32_t voffset)
+{
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void *)dst, 16,
+                                             (int)voffset, 0, 0, 0);
+}
+
+// Wait until at most N vector memory operations of this wave are outstanding
+// (they complete in issue order).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt()
+{
+    static_assert(N >= 0 && N < 64, "the counter has six bits");
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
 template <int I> struct Int {
     static constexpr int value = I;
 };
@@ -152,6 +196,16 @@ __device__ __forceinline__ void static_for(F &&f)
 __device__ __forceinline__ void lds_barrier()
 {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Workgroup barrier once this wave's LDS reads have returned, with no release
+// fence (which would also wait for the wave's global-to-LDS loads still in
+// flight); the acquire fence keeps later LDS accesses below it.
+__device__ __forceinline__ void stream_barrier()
+{
+    __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }

@@ -24,12 +24,12 @@ __device__ __forceinline__ uint64_t lds_load64(const uint64_t *p)
 // per SIMD. Each wave owns 16*RT consecutive rows of every
 // SCAN_WAVES*16*RT-row iteration and holds their inner products with all tile
 // queries in MFMA accumulators. Bank rows go from HBM straight into MFMA
-// operand registers (a ring of R k-steps, loads P k-steps ahead; the SIMD's
-// other wave covers the rest of the latency). Query fragments come from LDS:
-// the first GR query groups of the tile stay resident for the whole kernel;
-// the other groups stream through a double buffer one k-step at a time
-// (staged through registers two k-steps ahead), and only they need a
-// workgroup barrier per k-step. Candidates that pass a register-level test
+// operand registers (a ring of R k-steps, loads P = R - 1 k-steps ahead; the
+// SIMD's other wave covers the rest of the latency). Query fragments come
+// from LDS: the first GR query groups of the tile stay resident for the
+// whole kernel; the other groups stream from L2 by global-to-LDS loads into a
+// ring of R slots of one k-step each, also P k-steps ahead, and only they
+// need a workgroup barrier per k-step. Candidates that pass a register-level test
 // against the per-query bound go through per-wave staging into one list of
 // the k best per query shared by the workgroup, maintained with 64-bit
 // compare-and-swap so that the waves insert without locks.
@@ -42,19 +42,21 @@ __global__ __launch_bounds__(SCAN_THREADS, 1) void scan_kernel(const ScanArgs A)
     constexpr int KS = 4 * VEC;                    // elements of one k-step
     constexpr int RW = RT * 16;                    // rows per wave per iteration
     constexpr int RWG = SCAN_WAVES * RW;           // rows per workgroup iteration
-    constexpr int QPT = (NS * WAVE + SCAN_THREADS - 1) / SCAN_THREADS;   // stream items per thread
-    constexpr int R = scan_ring<NG>(), P = R - 1, QS = 2;
+    constexpr int R = scan_ring(DT, NG, GR, RAGGED), P = R - 1;
     static_assert(SCAN_KPAD % R == 0, "padded k-steps fill whole ring cycles");
     constexpr int NB = NG < 4 ? NG : 4;            // query fragments in flight
-    static_assert(P < R, "prefetch distance must leave a free ring slot");
-    static_assert(R % QS == 0 && R % 2 == 0, "staging slots and LDS buffers divide the unroll");
+    // streamed fragments of one k-step: wave w loads fragments w, w + 8, ...;
+    // every wave issues NDJ loads per k-step, those past the last fragment
+    // into a sink slot
+    constexpr int NDJ = (NS + SCAN_WAVES - 1) / SCAN_WAVES;
     static_assert(RW <= WAVE, "one bank-norm load per lane per iteration");
 
     extern __shared__ __align__(16) uint8_t smem[];
     const int k = A.k, nks = A.nks, nksp = A.nksp;
-    const ScanLayout L = scan_layout(NG, GR, nksp, k, RT);
+    const ScanLayout L = scan_layout(NG, GR, nksp, k, RT, R);
     const i32x4 *res = (const i32x4 *)(smem + L.res);
     i32x4 *strm = (i32x4 *)(smem + L.strm);
+    i32x4 *sink = strm + R * NS * WAVE;   // target of the loads past the last fragment
     uint64_t *list = (uint64_t *)(smem + L.list);
     float *qn_s = (float *)(smem + L.qn);
     uint32_t *gb_s = (uint32_t *)(smem + L.gb);
@@ -70,8 +72,9 @@ __global__ __launch_bounds__(SCAN_THREADS, 1) void scan_kernel(const ScanArgs A)
     const int c = (blockIdx.x / per8) * 8 + rem % 8;
     if (c >= A.n_chunks)
         return;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
     __builtin_assume(tid < SCAN_THREADS);
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: scalar branches on it
     const int col = lane & 15, jg = lane >> 4;
     const int q0 = t * BM;
     const long rbeg = (long)c * A.rows_per_chunk;
@@ -112,30 +115,26 @@ __global__ __launch_bounds__(SCAN_THREADS, 1) void scan_kernel(const ScanArgs A)
     const uint8_t *bank_c = A.bank + (size_t)rbeg * rowb;
     const uint32_t bank_c_bytes = (uint32_t)((rend - rbeg) * (long)rowb);
     const uint32_t q_bytes = (uint32_t)((size_t)A.B * rowb);
-    uint32_t qvo[QPT > 0 ? QPT : 1];   // per stream item: q*rowb + (l/16)*16, or OFF_NONE
-    int qkk[QPT > 0 ? QPT : 1];        // element offset of the item within a k-step
+    uint32_t dvo[NDJ > 0 ? NDJ : 1];   // per streamed fragment of this wave: q*rowb + (lane/16)*16
 #pragma unroll
-    for (int i = 0; i < QPT; ++i) {
-        const int item = tid + SCAN_THREADS * i;
-        const int f = item >> 6, l = item & 63;
-        const int q = q0 + (GR + f) * 16 + (l & 15);
-        qkk[i] = (l >> 4) * VEC;
-        qvo[i] = item < NS * WAVE && q < A.B ? (uint32_t)((size_t)q * rowb + (l >> 4) * 16)
-                                             : OFF_NONE;
+    for (int j = 0; j < NDJ; ++j) {
+        const int f = wave + SCAN_WAVES * j;
+        const int q = q0 + (GR + f) * 16 + col;
+        dvo[j] = f < NS && q < A.B ? (uint32_t)((size_t)q * rowb + jg * 16) : OFF_NONE;
     }
     int pq_s = 0;             // k-step of the next query load (every iteration is the same)
     int pb_it = 0, pb_s = 0;  // k-step of the next bank load
     uint32_t bvo = (uint32_t)((size_t)(wave * RW + col) * rowb + jg * 16);   // tile 0 of pb_it
-    auto issue_q = [&](i32x4(&qs)[QPT > 0 ? QPT : 1]) {
+    // this wave's streamed fragments of k-step pq_s into ring slot `slot`
+    auto issue_q = [&](int slot) {
         const bool real = pq_s < nks;
         const __amdgpu_buffer_rsrc_t r =
             make_rsrc(A.queries + pq_s * KSTEP_BYTES, real ? q_bytes - pq_s * KSTEP_BYTES : 0u);
+        const bool lane_ok = !RAGGED || pq_s * KS + jg * VEC < A.d;
 #pragma unroll
-        for (int i = 0; i < QPT; ++i) {
-            uint32_t vo = qvo[i];
-            if constexpr (RAGGED)
-                vo = pq_s * KS + qkk[i] < A.d ? vo : OFF_NONE;
-            qs[i] = buffer_load16(r, vo);
+        for (int j = 0; j < NDJ; ++j) {
+            const int f = wave + SCAN_WAVES * j;
+            dma16(r, f < NS ? strm + (slot * NS + f) * WAVE : sink, lane_ok ? dvo[j] : OFF_NONE);
         }
         if (++pq_s == nksp)
             pq_s = 0;
@@ -154,21 +153,16 @@ __global__ __launch_bounds__(SCAN_THREADS, 1) void scan_kernel(const ScanArgs A)
             bvo += (uint32_t)(RWG * rowb);
         }
     };
-    auto stage_queries = [&](int slot, const i32x4(&qs)[QPT > 0 ? QPT : 1]) {
-#pragma unroll
-        for (int i = 0; i < QPT; ++i) {
-            const int item = tid + SCAN_THREADS * i;
-            if (item < NS * WAVE)
-                strm[slot * NS * WAVE + item] = qs[i];
-        }
-    };
-    // -|x|^2/2 of bank row `lane` of this wave in iteration it (-inf past the chunk)
-    auto load_norm = [&](int it) -> float {
+    // |x|^2 of bank row `lane` of this wave in iteration it, and whether that
+    // row exists; its accumulator start -|x|^2/2 (-inf past the chunk) is
+    // formed an iteration later, so that no wait for the load holds up the
+    // loads in flight
+    auto load_norm = [&](int it, bool &ok) -> float {
         const long row = rbeg + (long)it * RWG + wave * RW + lane;
-        const bool v = lane < RW && it < n_it && row < rend;
-        const float xn = A.bank_norms[v ? row : 0];
-        return v ? -0.5f * xn : -INFINITY;
+        ok = lane < RW && it < n_it && row < rend;
+        return A.bank_norms[ok ? row : 0];
     };
+    auto norm_start = [](float xn, bool ok) -> float { return ok ? -0.5f * xn : -INFINITY; };
     // the bound of tile query i as a distance key: the shared bound or the
     // workgroup list's largest key, whichever is lower
     auto bound_key = [&](int i) -> uint32_t {
@@ -223,26 +217,31 @@ __global__ __launch_bounds__(SCAN_THREADS, 1) void scan_kernel(const ScanArgs A)
     };
     f32x4 acc[RT][NG];
     i32x4 ring[R][RT];
-    i32x4 qst[QS][QPT > 0 ? QPT : 1];
     int s_it = 0;   // k-step within the iteration
 
-    // One block of R k-steps.
-    // K-step x (counting over all iterations) reads stream buffer x & 1, which
-    // k-step x - 1 filled, and fills the other one for k-step x + 1 after a
-    // barrier that every wave reaches once it is done with k-step x - 1.
-    // Blocks start at multiples of R, so x & 1 = u & 1.
+    // One block of R k-steps. K-step x (counting over all iterations; blocks
+    // start at multiples of R, so x % R = u) uses bank ring slot u and stream
+    // slot u, both loaded at k-step x - P, and loads k-step x + P into the
+    // slots of k-step x - 1. Every k-step issues the same loads, in the same
+    // order (first the streamed fragments, then the bank rows), whether or not
+    // they fetch anything, so a fixed count of later loads tells when this
+    // wave's part of stream slot u has landed; the barrier after that wait
+    // tells that every wave's part has, and that every wave is done with
+    // k-step x - 1.
     auto block = [&]() {
 #pragma unroll
         for (int u = 0; u < R; ++u) {
             if constexpr (NS > 0) {
-                // (after the last k-step this fills a buffer nobody reads)
-                lds_barrier();
-                stage_queries((u + 1) & 1, qst[(u + 1) % QS]);
-                issue_q(qst[(u + 1) % QS]);
+                __builtin_amdgcn_sched_barrier(0);
+                wait_vmcnt<RT + (P - 1) * (NDJ + RT)>();
+                stream_barrier();
+                // (past the last k-step this loads slots nobody reads)
+                issue_q((u + P) % R);
+                __builtin_amdgcn_sched_barrier(0);
             }
             issue_b(ring[(u + P) % R]);
             const i32x4 *rb = res + s_it * GR * WAVE + lane;
-            const i32x4 *sb = strm + (u & 1) * NS * WAVE + lane;
+            const i32x4 *sb = strm + u * NS * WAVE + lane;
             auto frag = [&](int g) -> i32x4 { return g < GR ? rb[g * WAVE] : sb[(g - GR) * WAVE]; };
             i32x4 bq[NB];
 #pragma unroll
@@ -276,20 +275,27 @@ __global__ __launch_bounds__(SCAN_THREADS, 1) void scan_kernel(const ScanArgs A)
         refresh_nu(i);
     auto nu_read = [&](int i) -> float { return __uint_as_float(lds_load_relaxed(nu_s + i)); };
 
-    // ---- pipeline prologue
-#pragma unroll
-    for (int u = 0; u < P; ++u)
-        issue_b(ring[u]);
-    if constexpr (NS > 0) {
-#pragma unroll
-        for (int j = 0; j < QS; ++j)
-            issue_q(qst[j]);
-        stage_queries(0, qst[0]);
-        issue_q(qst[0]);
-    }
+    bool nx_ok;
+    const float nx0 = load_norm(0, nx_ok);
     if (lane < RW)
-        nx[lane] = load_norm(0);
-    float nx_next = load_norm(1);
+        nx[lane] = norm_start(nx0, nx_ok);
+
+    // ---- pipeline prologue: k-steps 0 .. P-1, in the steady-state order
+#pragma unroll
+    for (int u = 0; u < P; ++u) {
+        if constexpr (NS > 0) {
+            __builtin_amdgcn_sched_barrier(0);
+            issue_q(u);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        issue_b(ring[u]);
+    }
+    float nx_next = load_norm(1, nx_ok);
+    // the shared bound of tile query tid as the next refresh takes it (loaded
+    // an iteration ahead for the same reason)
+    static_assert(BM <= SCAN_THREADS, "one tile query per thread");
+    const bool own_q = tid < BM && q0 + tid < A.B;
+    uint32_t tau_next = own_q ? A.tau[q0 + tid] : KEY_NONE;
     __syncthreads();
 
     for (int it = 0; it < n_it; ++it) {
@@ -302,13 +308,16 @@ __global__ __launch_bounds__(SCAN_THREADS, 1) void scan_kernel(const ScanArgs A)
                 acc[tt][g] = nxh;
         }
         s_it = 0;
-        for (int s0 = 0; s0 < nksp; s0 += R)
+        int s0 = 0;
+        do {   // (nksp >= R: the loads of at least one block follow those before it)
             block();
+            s0 += R;
+        } while (s0 < nksp);
 
         // ---- end of iteration `it`: acc = -|x|^2/2 + <q, x>; dist = |q|^2 - 2*acc
         if (lane < RW)
-            nx[((it + 1) & 1) * RW + lane] = nx_next;
-        nx_next = load_norm(it + 2);
+            nx[((it + 1) & 1) * RW + lane] = norm_start(nx_next, nx_ok);
+        nx_next = load_norm(it + 2, nx_ok);
         // Phase 1: stage every candidate of this iteration, in (group, tile,
         // element, lane) order, in LDS and past STAGE_CAP in this wave's
         // overflow area (an iteration has at most RW*BM of them).
@@ -385,16 +394,22 @@ __global__ __launch_bounds__(SCAN_THREADS, 1) void scan_kernel(const ScanArgs A)
             }
             insert_lanes(s < nst, vi, vk, vx);
         }
-        // pick up bounds other workgroups have lowered
-        for (int i = tid; i < BM; i += SCAN_THREADS) {
-            if (q0 + i < A.B)
-                lds_store_relaxed(gb_s + i, __hip_atomic_load(A.tau + q0 + i, __ATOMIC_RELAXED,
-                                                              __HIP_MEMORY_SCOPE_AGENT));
-            refresh_nu(i);
+        // pick up bounds other workgroups have lowered (as of the previous
+        // iteration: the shared bound only decreases, so any value of it is
+        // a bound)
+        if (tid < BM) {
+            if (own_q)
+                lds_store_relaxed(gb_s + tid, tau_next);
+            refresh_nu(tid);
+            if (own_q)
+                tau_next = __hip_atomic_load(A.tau + q0 + tid, __ATOMIC_RELAXED,
+                                             __HIP_MEMORY_SCOPE_AGENT);
         }
     }
 
     // ---- the workgroup's lists -> workspace [B][n_chunks][k], valid entries first
+    // (no global-to-LDS load may still be in flight when the workgroup ends)
+    wait_vmcnt<0>();
     __syncthreads();
     for (int i = wave; i < BM; i += SCAN_WAVES) {
         const int q = q0 + i;
@@ -438,6 +453,9 @@ hipError_t launch_scan_g(const KnnPlan &p, const ScanArgs &a, int grid, hipStrea
     if constexpr (NG >= 4)
         if (p.gr == NG / 4)
             return launch_scan<DT, NG, NG / 4, RAGGED>(a, p.lds_bytes, grid, s);
+    if constexpr (NG >= 8)
+        if (p.gr == NG / 8)
+            return launch_scan<DT, NG, NG / 8, RAGGED>(a, p.lds_bytes, grid, s);
     if (p.gr == 0)
         return launch_scan<DT, NG, 0, RAGGED>(a, p.lds_bytes, grid, s);
     return hipErrorInvalidValue;

@@ -84,6 +84,11 @@ KNN_CASES = [
     ("bf16", 40, 64, 40, 33),       # fewer rows than chunks can use
     ("bf16", 256, 600, 768, 10),    # no seed sample (N < 64k): every pair of the first
                                     # iteration is a candidate, most past the LDS staging
+    # batches of 65..256 requests with d = 768 take the query-resident scan
+    ("bf16", 100, 50000, 768, 10),  # a partly filled wave and idle waves
+    ("bf16", 200, 100003, 768, 16), # its largest k; chunks that end inside a block
+    ("bf16", 129, 70000, 768, 1),   # k = 1
+    ("bf16", 200, 9000, 768, 17),   # k past its limit: the tile scan again
 ]
 
 
