@@ -41,8 +41,8 @@ constexpr int SEED_MAX_GROUPS = 2048;  // S / 16 for S <= 32768
 constexpr int RQ_WAVES = 8;
 constexpr int RQ_QW = 2;
 constexpr int RQ_ROWS = 32;
-constexpr int RQ_KSTG = 8;
-constexpr int RQ_STAGES = 7;
+constexpr int RQ_KSTG = 24;
+constexpr int RQ_STAGES = 2;
 constexpr int RQ_NKS = 24;
 constexpr int RQ_MAX_K = 16;
 
