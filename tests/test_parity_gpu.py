@@ -89,6 +89,8 @@ KNN_CASES = [
     ("bf16", 200, 100003, 768, 16), # its largest k; chunks that end inside a block
     ("bf16", 129, 70000, 768, 1),   # k = 1
     ("bf16", 200, 9000, 768, 17),   # k past its limit: the tile scan again
+    ("bf16", 70, 20, 768, 10),      # fewer bank rows than one of its 32-row blocks
+    ("bf16", 65, 1, 768, 1),        # its smallest batch, a single bank row
 ]
 
 
