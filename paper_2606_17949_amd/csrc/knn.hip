@@ -174,24 +174,42 @@ __global__ __launch_bounds__(SEED_WAVES * WAVE) void seed_groups_kernel(const Se
     }
 }
 
-// One workgroup of SEED_BOUND_WAVES waves per query: |q|^2, and the starting
-// bound = |q|^2 + the k-th smallest group minimum, widened by a margin far
-// above any fp32 rounding difference between this pass and the scan. The
-// k-th smallest is found bit by bit from the top: each wave counts its share
-// of the group minima below the trial value, and the workgroup adds the four
-// counts through LDS (one barrier per bit). Without a seed (G < k) the bound
-// is +inf.
-constexpr int SEED_BOUND_WAVES = 4;
-
+// One wave per query: |q|^2, and the starting bound = |q|^2 + the k-th
+// smallest of the wave's 128 lane values (each lane's two smallest group
+// minima; lane l holds groups l, l + 64, ...), widened by a margin far above
+// any fp32 rounding difference between this pass and the scan. The values
+// belong to distinct groups, so the k smallest are distances of k distinct
+// sample rows and bound the k-th nearest distance from above; they are the
+// k smallest group minima unless three of those share a lane. The k-th
+// smallest is found bit by bit from the top, two ballots per bit. Without a
+// seed (G < k) the bound is +inf.
 template <int DT, int GPL>
-__global__ __launch_bounds__(SEED_BOUND_WAVES * WAVE) void seed_bound_kernel(
-    const uint8_t *__restrict__ queries, int B, int d, int k, const float *__restrict__ gmin,
-    int G, float *__restrict__ qn, uint32_t *__restrict__ tau)
+__global__ __launch_bounds__(WAVE) void seed_bound_kernel(const uint8_t *__restrict__ queries,
+                                                          int B, int d, int k,
+                                                          const float *__restrict__ gmin, int G,
+                                                          float *__restrict__ qn,
+                                                          uint32_t *__restrict__ tau)
 {
-    static_assert(GPL * WAVE * SEED_BOUND_WAVES >= SEED_MAX_GROUPS, "every group has a slot");
-    __shared__ int cnt[2][SEED_BOUND_WAVES];
-    const int lane = lane_id(), wave = threadIdx.x >> 6;
+    static_assert(GPL * WAVE >= SEED_MAX_GROUPS, "every group has a slot");
+    const int lane = lane_id();
     const int b = blockIdx.x;
+    // every load in flight at once: slots past G read the last group and
+    // discard it
+    uint32_t m1 = KEY_NONE, m2 = KEY_NONE;   // the lane's smallest and second smallest
+    if (G >= k) {
+        uint32_t key[GPL];
+#pragma unroll
+        for (int u = 0; u < GPL; ++u) {
+            const int i = u * WAVE + lane;
+            const float v = gmin[(size_t)b * G + (i < G ? i : G - 1)];
+            key[u] = f2key(v) | (i < G ? 0u : KEY_NONE);   // uses v unconditionally
+        }
+#pragma unroll
+        for (int u = 0; u < GPL; ++u) {
+            m2 = min(m2, max(m1, key[u]));
+            m1 = min(m1, key[u]);
+        }
+    }
     const int row_bytes = d * Elem<DT>::ESZ;
     const uint8_t *row = queries + (size_t)b * row_bytes;
     float s = 0.f;
@@ -200,31 +218,12 @@ __global__ __launch_bounds__(SEED_BOUND_WAVES * WAVE) void seed_bound_kernel(
     s = wave_sum(s);
     uint32_t T = KEY_NONE;
     if (G >= k) {
-        // every load in flight at once: slots past G read the last group and
-        // discard it
-        uint32_t key[GPL];
-#pragma unroll
-        for (int u = 0; u < GPL; ++u) {
-            const int i = (wave * GPL + u) * WAVE + lane;
-            const float v = gmin[(size_t)b * G + (i < G ? i : G - 1)];
-            key[u] = f2key(v) | (i < G ? 0u : KEY_NONE);   // uses v unconditionally
-        }
+        // the largest prefix with fewer than k lane values below it is the
+        // k-th smallest lane value (the lanes hold min(G, 128) >= k groups)
         uint32_t prefix = 0;
         for (int bit = 31; bit >= 0; --bit) {
             const uint32_t trial = prefix | (1u << bit);
-            int c = 0;
-#pragma unroll
-            for (int u = 0; u < GPL; ++u)
-                c += key[u] < trial;
-            const int wc = (int)wave_sum((float)c);
-            if (lane == 0)
-                cnt[bit & 1][wave] = wc;
-            __syncthreads();   // (the other buffer is rewritten only after the next barrier)
-            int total = 0;
-#pragma unroll
-            for (int w = 0; w < SEED_BOUND_WAVES; ++w)
-                total += cnt[bit & 1][w];
-            if (total < k)
+            if (popc(ballot(m1 < trial)) + popc(ballot(m2 < trial)) < k)
                 prefix = trial;
         }
         const float pk = key2f(prefix);
@@ -232,7 +231,7 @@ __global__ __launch_bounds__(SEED_BOUND_WAVES * WAVE) void seed_bound_kernel(
         const float margin = ldexpf(s + fabsf(pk) + 1.f, -14);
         T = f2key(t + margin);
     }
-    if (threadIdx.x == 0) {
+    if (lane == 0) {
         qn[b] = s;
         tau[b] = T;
     }
@@ -320,32 +319,33 @@ __global__ __launch_bounds__(MERGE_WAVES * WAVE) void merge_kernel(const MergeAr
     const int k = A.k, W = A.W;
     const int32_t *cnt = A.ccnt + (size_t)b * W;
     const size_t base = (size_t)b * W * k;
+    // the first GE entries of every list of this lane are loaded with the
+    // list lengths, whatever the lengths (lists are short once the bound is
+    // tight; a lane past the last list reads the last list); longer lists
+    // finish after
+    constexpr int GE = LPL <= 8 ? 4 : 1;
+    uint32_t kk[LPL][GE];
+    int32_t ii[LPL][GE];
     int n[LPL], mine = 0;
 #pragma unroll
     for (int u = 0; u < LPL; ++u) {
         const int w = lane + WAVE * u;
         n[u] = w < W ? cnt[w] : 0;
-        mine += n[u];
+        const size_t o = base + (size_t)min(w, W - 1) * k;
+#pragma unroll
+        for (int j = 0; j < GE; ++j) {
+            kk[u][j] = j < k ? A.ckey[o + j] : 0u;
+            ii[u][j] = j < k ? A.cidx[o + j] : 0;
+        }
     }
+#pragma unroll
+    for (int u = 0; u < LPL; ++u)
+        mine += n[u];
     const int incl = wave_incl_scan(mine);
     const int total = __builtin_amdgcn_readlane(incl, WAVE - 1);
     const bool in_lds = total <= MERGE_CAP;
     if (in_lds) {
-        // the first GE entries of every list of this lane are loaded together
-        // (lists are short once the bound is tight); longer lists finish after
-        constexpr int GE = LPL <= 8 ? 4 : 1;
         int off = incl - mine;
-        uint32_t kk[LPL][GE];
-        int32_t ii[LPL][GE];
-#pragma unroll
-        for (int u = 0; u < LPL; ++u) {
-            const size_t o = base + (size_t)(lane + WAVE * u) * k;
-#pragma unroll
-            for (int j = 0; j < GE; ++j) {
-                kk[u][j] = j < n[u] ? A.ckey[o + j] : 0u;
-                ii[u][j] = j < n[u] ? A.cidx[o + j] : 0;
-            }
-        }
 #pragma unroll
         for (int u = 0; u < LPL; ++u) {
             const size_t o = base + (size_t)(lane + WAVE * u) * k;
@@ -399,9 +399,45 @@ __global__ __launch_bounds__(MERGE_WAVES * WAVE) void merge_kernel(const MergeAr
             nbr[lane] = pidx;
             wts[lane] = inv_dist_weight(key2f((uint32_t)(pick >> 32)));
         }
-        for (int m = lane; m < A.M; m += WAVE)
-            average_labels(nbr, A.inv_dist ? wts : nullptr, k, A.qual, A.len, A.N, A.M, m,
-                           A.q_hat + (size_t)b * A.M + m, A.l_hat + (size_t)b * A.M + m);
+        const int M = A.M;
+        if (k * M <= WAVE) {
+            // every (neighbour, model) label in flight at once: lane j*M + m
+            // loads neighbour j's labels for model m; lane m then adds them
+            // up in neighbour order exactly as average_labels does
+            const int jl = lane / M, ml = lane - jl * M;
+            const bool own = lane < k * M;
+            const int32_t nj = __shfl(pidx, own ? jl : 0);
+            const bool ok = nj >= 0 && nj < A.N;
+            const size_t o = (size_t)(ok ? nj : 0) * M + (own ? ml : 0);
+            const float qv = A.qual[o], lv = A.len[o];
+            const int mm = lane < M ? lane : 0;
+            float sq = 0.f, sl = 0.f, sw = 0.f;
+            bool bad = false;
+            for (int j = 0; j < k; ++j) {
+                const int src = j * M + mm;
+                const float q = __shfl(qv, src), l = __shfl(lv, src);
+                bad |= __shfl((int)ok, src) == 0;
+                if (A.inv_dist) {
+                    const float w = wts[j];
+                    sq = fmaf(w, q, sq);
+                    sl = fmaf(w, l, sl);
+                    sw += w;
+                } else {
+                    sq += q;
+                    sl += l;
+                }
+            }
+            if (!A.inv_dist)
+                sw = (float)k;
+            if (lane < M) {
+                A.q_hat[(size_t)b * M + lane] = bad ? __builtin_nanf("") : sq / sw;
+                A.l_hat[(size_t)b * M + lane] = bad ? __builtin_nanf("") : sl / sw;
+            }
+        } else {
+            for (int m = lane; m < M; m += WAVE)
+                average_labels(nbr, A.inv_dist ? wts : nullptr, k, A.qual, A.len, A.N, M, m,
+                               A.q_hat + (size_t)b * M + m, A.l_hat + (size_t)b * M + m);
+        }
     }
 }
 
@@ -450,8 +486,8 @@ hipError_t launch_seed_bound(const KnnPlan &p, const void *queries, const float 
 {
     const uint8_t *q = (const uint8_t *)queries;
     const int G = p.S ? p.G : 0;
-    constexpr int GPL = SEED_MAX_GROUPS / (WAVE * SEED_BOUND_WAVES);
-    hipLaunchKernelGGL((seed_bound_kernel<DT, GPL>), dim3(p.B), dim3(SEED_BOUND_WAVES * WAVE), 0, s,
+    constexpr int GPL = SEED_MAX_GROUPS / WAVE;
+    hipLaunchKernelGGL((seed_bound_kernel<DT, GPL>), dim3(p.B), dim3(WAVE), 0, s,
                        q, p.B, p.d, p.k, gmin, G, qn, tau);
     return hipGetLastError();
 }
