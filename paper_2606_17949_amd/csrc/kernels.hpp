@@ -48,9 +48,10 @@ constexpr int RQ_MAX_K = 16;
 
 // How one rb_knn_topk call is split (the tile scan; the query-resident scan
 // differs in that one workgroup holds the whole batch, so n_qt = 1).
-//  * seed: S bank rows spread evenly over the bank; per query, the k-th
-//    smallest of the S/16 minima over groups of 16 of them bounds the k-th
-//    nearest distance from above (k distinct rows lie at or below it).
+//  * seed: S bank rows spread evenly over the bank, scored in groups of 16;
+//    per query, the k-th smallest of 128 of the S/16 group minima (each
+//    lane's two smallest of its share) bounds the k-th nearest distance from
+//    above (k distinct rows lie at or below it).
 //  * scan: query tiles of 16*ng queries, whose first gr groups stay in LDS
 //    for the whole call while the others stream through it; the
 //    bank in n_chunks contiguous row ranges (multiples of 16 rows); one
