@@ -82,8 +82,11 @@ KNN_CASES = [
     ("bf16", 33, 3000, 2048, 10),   # largest d
     ("f32", 20, 500, 2048, 5),      # largest d, fp32
     ("bf16", 40, 64, 40, 33),       # fewer rows than chunks can use
-    ("bf16", 256, 600, 768, 10),    # no seed sample (N < 64k): every pair of the first
-                                    # iteration is a candidate, most past the LDS staging
+    ("bf16", 256, 150, 512, 10),    # no seed (8 sample groups < k): every pair of the
+                                    # first iteration is a candidate, most past the LDS staging
+    # the seed bound's wave holds each lane's two smallest group minima
+    ("bf16", 100, 700, 768, 20),    # 40 groups: fewer than the wave's lanes
+    ("bf16", 100, 1600, 768, 64),   # 100 groups, one or two per lane, largest k
     # batches of 65..256 requests with d = 768 take the query-resident scan
     ("bf16", 100, 50000, 768, 10),  # a partly filled wave and idle waves
     ("bf16", 200, 100003, 768, 16), # its largest k; chunks that end inside a block
@@ -91,6 +94,8 @@ KNN_CASES = [
     ("bf16", 200, 9000, 768, 17),   # k past its limit: the tile scan again
     ("bf16", 70, 20, 768, 10),      # fewer bank rows than one of its 32-row blocks
     ("bf16", 65, 1, 768, 1),        # its smallest batch, a single bank row
+    ("bf16", 256, 600, 768, 10),    # a full batch with a 36-group seed
+    ("bf16", 200, 4096, 768, 16),   # 128 seed groups: exactly two per lane of the bound
 ]
 
 
