@@ -78,7 +78,8 @@ class Config:
 
 # The five workloads: a tiny one the oracle finishes in seconds, the paper-scale
 # online batch, a high-load batch (carried over 100 batches), a compute-bound
-# large batch and a wide cluster.
+# large batch and a wide cluster; and stream64, the online batch of 64 requests
+# over the high-load bank, an HBM-scale stream of a small batch.
 CONFIGS = {
     "tiny": Config("tiny", B=16, N=2048, d=384, dtype="f32", clusters=32, M=4,
                    inst_per_model=(5, 4, 2, 2), weights=(0.4, 0.3, 0.3)),
@@ -89,6 +90,8 @@ CONFIGS = {
     "largebatch": Config("largebatch", B=1024, N=1_000_000, d=1024, dtype="bf16", clusters=1024,
                          M=8, inst_per_model=(8,) * 8, weights=(0.5, 0.25, 0.25),
                          qual_alpha0=1.5, qual_alpha_step=0.5),
+    "stream64": Config("stream64", B=64, N=1_000_000, d=768, dtype="bf16", clusters=1024, M=4,
+                       inst_per_model=(5, 4, 2, 2), weights=(0.4, 0.3, 0.3)),
     "wide": Config("wide", B=512, N=4_000_000, d=384, dtype="bf16", clusters=4096, M=16,
                    inst_per_model=(32,) * 16, weights=(0.1, 0.2, 0.7),
                    len_mu0=5.5, len_mu_step=0.0, len_sigma=1.0, prompt_mu=7.0, prompt_sigma=1.0),

@@ -330,7 +330,7 @@ def test_route_batch_end_to_end(name, over):
 
 
 @pytest.mark.parametrize("name,sample", [("online", None), ("highload", 8), ("largebatch", 4),
-                                         ("wide", 4)])
+                                         ("wide", 4), ("stream64", 8)])
 def test_full_size_sampled_parity(name, sample):
     """The workloads at their real sizes, in the configuration the benchmark
     times. The oracle recomputes every prediction, score and pick (teacher
