@@ -45,6 +45,8 @@ TRAFFIC_FILE = "profiles/scan_traffic.json"
 # SCAN_EVENT_EVERY-th batch of the timed run (each event record adds a few
 # microseconds of queue work to the stream it is recorded on).
 SCAN_EVENT_EVERY = 8
+# Workspaces of the pipelined schedule, used in turn.
+WS_RING = 8
 
 
 def scan_source_digest():
@@ -86,8 +88,9 @@ def parse():
     ap.add_argument("--options", default="",
                     help="comma list of lpt, inv_dist, budget, mask (rb_route_batch_ex)")
     ap.add_argument("--schedule", choices=("pipelined", "sequential"), default="pipelined",
-                    help="pipelined: the KNN lookup of batch t+1 runs on a second stream while "
-                         "batch t is assigned; sequential: one rb_route_batch call per batch")
+                    help="pipelined: the seed and bank scan of batch t+1 run on a second stream "
+                         "while batch t is merged, averaged and assigned; sequential: one "
+                         "rb_route_batch call per batch")
     ap.add_argument("--cpu-sample", type=int, default=0,
                     help="requests in the CPU oracle sample (0: 8 per host thread)")
     ap.add_argument("--record-traffic", metavar="PMC_DIR",
@@ -262,33 +265,48 @@ def main():
                                  cfg.weights, opts[t], ws=ws, assign=assign[t], stream=stream)
         rb.rb_advance_state(inst, carry_dt, stream=stream)
 
-    # pipelined schedule: lookups on s_knn, greedy passes and carries in batch
-    # order on s_asg; greedy pass t waits for lookup t. Each batch has its own
-    # prediction buffers (B*M*8 bytes), so no lookup waits for a greedy pass:
-    # a wait between streams costs the lookup stream several microseconds of
-    # queue work per batch even when the event has long completed.
+    # pipelined schedule: the first half of each lookup (seed and bank scan,
+    # RB_FLAG_LISTS_ONLY) on s_knn; the second half (merge of the chunk lists
+    # and label average, RB_FLAG_FROM_LISTS), the greedy pass and the carry in
+    # batch order on s_asg, after an event on the first half. A ring of
+    # WS_RING workspaces: a lookup waits for the merge WS_RING batches back,
+    # which last read its workspace. The greedy stream keeps a few hundred
+    # microseconds of slack per batch, but a merge that finds every compute
+    # unit taken by the next scan waits for the few units the scan leaves
+    # free, so the ring is deep enough that such a late merge never holds up
+    # a lookup.
     s_knn = torch.cuda.Stream(device=dev)
     s_asg = torch.cuda.Stream(device=dev) if args.schedule == "pipelined" else stream
-    qh = [torch.empty(cfg.B, cfg.M, device=dev) for _ in range(nb)]
-    lh = [torch.empty(cfg.B, cfg.M, device=dev) for _ in range(nb)]
+    n_ws = WS_RING if args.schedule == "pipelined" else 1
+    wss = [ws] + [rb.workspace(cfg.B, cfg.N, cfg.d, dt_code, cfg.k, cfg.M, dev)
+                  for _ in range(n_ws - 1)]
+    qh = torch.empty(cfg.B, cfg.M, device=dev)
+    lh = torch.empty(cfg.B, cfg.M, device=dev)
     order_buf = torch.empty(cfg.B, dtype=torch.int32, device=dev)
     wmode = rb.RB_KNN_INV_DIST if "inv_dist" in opt_names else rb.RB_KNN_UNIFORM
-    knn_opts = rb.options(weighting=wmode, flags=rb.RB_FLAG_OVERLAP)
+    lists_opts = rb.options(weighting=wmode, flags=rb.RB_FLAG_OVERLAP | rb.RB_FLAG_LISTS_ONLY)
+    merge_opts = rb.options(weighting=wmode, flags=rb.RB_FLAG_OVERLAP | rb.RB_FLAG_FROM_LISTS)
     lpt = "lpt" in opt_names
     asg_opts = [rb.options(order=rb.RB_ORDER_LPT if lpt else rb.RB_ORDER_ARRIVAL,
                            budget=budgets[t], instance_mask=mask,
                            order_out=order_buf if lpt else None)
                 for t in range(nb)]
     ev_knn = [torch.cuda.Event() for _ in range(nb)]
+    ev_mrg = [torch.cuda.Event() for _ in range(nb)]
 
     def lookup(t):
-        rb.rb_knn_predict(queries[t], bank, norms, cfg.k, g_qual, g_len, knn_opts, ws=ws,
-                          q_hat=qh[t], l_hat=lh[t], stream=s_knn)
+        if t >= n_ws:
+            s_knn.wait_event(ev_mrg[t - n_ws])
+        rb.rb_knn_predict(queries[t], bank, norms, cfg.k, g_qual, g_len, lists_opts,
+                          ws=wss[t % n_ws], stream=s_knn)
         ev_knn[t].record(s_knn)
 
     def decide(t):
         s_asg.wait_event(ev_knn[t])
-        rb.rb_assign_ex(qh[t], lh[t], plens[t], inst, cfg.weights, asg_opts[t],
+        rb.rb_knn_predict(queries[t], bank, norms, cfg.k, g_qual, g_len, merge_opts,
+                          ws=wss[t % n_ws], q_hat=qh, l_hat=lh, stream=s_asg)
+        ev_mrg[t].record(s_asg)
+        rb.rb_assign_ex(qh, lh, plens[t], inst, cfg.weights, asg_opts[t],
                         assign=assign[t], stream=s_asg, want_chosen=False)
         rb.rb_advance_state(inst, carry_dt, stream=s_asg)
 
@@ -412,8 +430,9 @@ def main():
                    "parallelism": "single GPU"},
         "options": opt_names,
         "schedule": args.schedule if args.schedule == "sequential" else
-        "pipelined: the KNN lookup of batch t+1 (second stream) overlaps the greedy pass of "
-        "batch t; every batch's lookup, greedy pass and carry are inside the timed region",
+        "pipelined: the seed and bank scan of batch t+1 (second stream) overlap the merge, "
+        "greedy pass and carry of batch t; every batch's lookup, greedy pass and carry are "
+        "inside the timed region",
         "bank_scan_gbps": round(scan_gbs, 1),
         "arith_intensity_flop_per_byte": round(ai, 1),
         "roofline": roof,

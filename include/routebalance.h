@@ -201,6 +201,20 @@ rb_status rb_assign(const float *q_hat, const float *l_hat, const int32_t *promp
  *     bank whose rows per unit would pass 2 GB is split further and may
  *     leave none free). Results do not change. */
 #define RB_FLAG_OVERLAP 1u
+/*   RB_FLAG_LISTS_ONLY, RB_FLAG_FROM_LISTS (rb_knn_predict only, not both):
+ *     the lookup in two calls, so that its two halves can go on different
+ *     streams. With RB_FLAG_LISTS_ONLY the call runs the seed and the bank
+ *     scan and leaves the per-chunk candidate lists in the workspace; it
+ *     writes none of nbr_idx, nbr_dist, q_hat, l_hat (q_hat and l_hat may
+ *     then be NULL). With RB_FLAG_FROM_LISTS it runs only the merge of those
+ *     lists and the label average, from the lists that the last
+ *     RB_FLAG_LISTS_ONLY call on this workspace left there; that call must
+ *     have had the same dtype, B, N, d, k and RB_FLAG_OVERLAP bit, on the same
+ *     device, and have completed (same stream, or ordered before this call by
+ *     an event). The queries and the bank are then not read. The two calls
+ *     give the same outputs as one call without either flag. */
+#define RB_FLAG_LISTS_ONLY 2u
+#define RB_FLAG_FROM_LISTS 4u
 
 /* Options of rb_assign_ex, rb_knn_predict and rb_route_batch_ex (a host
  * struct; the pointers are device pointers). A zero-initialised struct (or a
@@ -219,7 +233,8 @@ rb_status rb_assign(const float *q_hat, const float *l_hat, const int32_t *promp
  *                  order_out[t] = request decided at step t. Required by
  *                  rb_assign_ex when order is RB_ORDER_LPT (it also serves as
  *                  that call's scratch); optional for rb_route_batch_ex.
- *   flags          RB_FLAG_* bits; other bits must be 0.
+ *   flags          RB_FLAG_* bits (the two split flags for rb_knn_predict
+ *                  only); other bits must be 0.
  * The candidate set of a request is the available, admitted instances; Eq. 1's
  * cost and latency maxima run over it (Sec. 4.1: normalised by the candidates'
  * maxima) and the argmax is taken within it. A request with an empty candidate
@@ -261,14 +276,16 @@ rb_status rb_route_batch(const void *queries, const void *bank, const float *ban
  * call. Nothing here reads the instance state, so the lookup of the next
  * batch can run on one stream while rb_assign_ex decides the current batch on
  * another (with RB_FLAG_OVERLAP the scan leaves room for it).
- *   q_hat, l_hat [B][M] fp32 (outputs, required); nbr_idx, nbr_dist [B][k]
- *   (outputs, may be NULL: then kept in the workspace); opts may be NULL; its
- *   order, budget, instance_mask and order_out are not read.
+ *   q_hat, l_hat [B][M] fp32 (outputs, required but with RB_FLAG_LISTS_ONLY);
+ *   nbr_idx, nbr_dist [B][k] (outputs, may be NULL: then kept in the
+ *   workspace); opts may be NULL; its order, budget, instance_mask and
+ *   order_out are not read; its flags may also hold RB_FLAG_LISTS_ONLY or
+ *   RB_FLAG_FROM_LISTS (the lookup split in two calls).
  *   ws: as for rb_route_batch (rb_workspace_size bytes); the call uses only
  *   its own workspace, so concurrent calls need distinct workspaces.
  * Errors: as rb_knn_topk, plus RB_ERR_DIMS (M < 1, M > RB_MAX_M), RB_ERR_NULL
  * (bank_qual, bank_len, q_hat, l_hat), RB_ERR_UNSUPPORTED (weighting or
- * flags out of range). */
+ * flags out of range, or both split flags). */
 rb_status rb_knn_predict(const void *queries, const void *bank, const float *bank_norms,
                          rb_dtype dtype, int B, int N, int d, int k, const float *bank_qual,
                          const float *bank_len, int M, const rb_options *opts, int32_t *nbr_idx,

@@ -25,7 +25,7 @@ RB_ERR_WORKSPACE, RB_ERR_UNSUPPORTED, RB_ERR_HIP, RB_ERR_ALIGN = -5, -6, -7, -8
 RB_F32, RB_BF16 = 0, 1
 RB_KNN_UNIFORM, RB_KNN_INV_DIST = 0, 1
 RB_ORDER_ARRIVAL, RB_ORDER_LPT = 0, 1
-RB_FLAG_OVERLAP = 1
+RB_FLAG_OVERLAP, RB_FLAG_LISTS_ONLY, RB_FLAG_FROM_LISTS = 1, 2, 4
 RB_MAX_K, RB_MAX_D, RB_MAX_I, RB_MAX_M = 64, 2048, 1024, 1024
 
 # every symbol include/routebalance.h declares
@@ -340,14 +340,20 @@ def rb_knn_predict(queries, bank, bank_norms, k: int, bank_qual, bank_len,
                    q_hat: Optional[torch.Tensor] = None, l_hat: Optional[torch.Tensor] = None,
                    nbr_idx: Optional[torch.Tensor] = None, nbr_dist: Optional[torch.Tensor] = None,
                    stream=None):
-    """KNN lookup and label average in one call: returns (q_hat, l_hat)."""
+    """KNN lookup and label average in one call: returns (q_hat, l_hat).
+
+    With RB_FLAG_LISTS_ONLY in ``opts.flags`` only the seed and the bank scan
+    run (their lists stay in ``ws``; returns (None, None) unless buffers are
+    given); with RB_FLAG_FROM_LISTS only the merge and average of the lists a
+    LISTS_ONLY call left in ``ws`` (the same shapes and overlap flag)."""
     B, d = queries.shape
     N = bank.shape[0]
     M = bank_qual.shape[1]
     dev = queries.device
-    if q_hat is None:
+    lists_only = opts is not None and (opts.flags & RB_FLAG_LISTS_ONLY)
+    if q_hat is None and not lists_only:
         q_hat = torch.empty(B, M, dtype=torch.float32, device=dev)
-    if l_hat is None:
+    if l_hat is None and not lists_only:
         l_hat = torch.empty(B, M, dtype=torch.float32, device=dev)
     if ws is None:
         ws = workspace(B, N, d, _dtype_code(bank), k, M, dev)

@@ -122,13 +122,16 @@ RouteExtra route_extra(size_t base, int B, int k, int M)
 const rb_options k_default_opts = {RB_ORDER_ARRIVAL, RB_KNN_UNIFORM, nullptr, nullptr, nullptr,
                                    0u};
 
-rb_status check_opts(const rb_options *o)
+// `flags_ok`: the flag bits the entry point takes.
+rb_status check_opts(const rb_options *o, uint32_t flags_ok = RB_FLAG_OVERLAP)
 {
     if (o->order != RB_ORDER_ARRIVAL && o->order != RB_ORDER_LPT)
         return RB_ERR_UNSUPPORTED;
     if (o->weighting != RB_KNN_UNIFORM && o->weighting != RB_KNN_INV_DIST)
         return RB_ERR_UNSUPPORTED;
-    if (o->flags & ~RB_FLAG_OVERLAP)
+    if (o->flags & ~flags_ok)
+        return RB_ERR_UNSUPPORTED;
+    if ((o->flags & RB_FLAG_LISTS_ONLY) && (o->flags & RB_FLAG_FROM_LISTS))
         return RB_ERR_UNSUPPORTED;
     return RB_OK;
 }
@@ -390,13 +393,18 @@ rb_status rb_knn_predict(const void *queries, const void *bank, const float *ban
         return s;
     if (M < 1 || M > RB_MAX_M)
         return RB_ERR_DIMS;
-    if ((s = check_opts(o)) != RB_OK)
+    if ((s = check_opts(o, RB_FLAG_OVERLAP | RB_FLAG_LISTS_ONLY | RB_FLAG_FROM_LISTS)) != RB_OK)
         return s;
     if (B == 0)
         return RB_OK;
-    if (!queries || !bank || !bank_norms || !bank_qual || !bank_len || !q_hat || !l_hat)
+    // the halves of the lookup: seed and scan to the lists, then merge and average
+    const bool lists_only = (o->flags & RB_FLAG_LISTS_ONLY) != 0;
+    const bool from_lists = (o->flags & RB_FLAG_FROM_LISTS) != 0;
+    if (!from_lists && (!queries || !bank || !bank_norms))
         return RB_ERR_NULL;
-    if (!aligned(queries, 16) || !aligned(bank, 16))
+    if (!lists_only && (!bank_qual || !bank_len || !q_hat || !l_hat))
+        return RB_ERR_NULL;
+    if (!from_lists && (!aligned(queries, 16) || !aligned(bank, 16)))
         return RB_ERR_ALIGN;
     rb::KnnPlan p;
     if ((s = plan(B, N, d, dtype, k, &p, (o->flags & RB_FLAG_OVERLAP) != 0)) != RB_OK)
@@ -407,9 +415,11 @@ rb_status rb_knn_predict(const void *queries, const void *bank, const float *ban
     if (!aligned(ws, 256))
         return RB_ERR_ALIGN;
     int32_t *nbr = nbr_idx ? nbr_idx : (int32_t *)((uint8_t *)ws + ex.off_nbr);
+    const int phases = lists_only ? rb::KNN_LISTS : from_lists ? rb::KNN_MERGE : rb::KNN_ALL;
     return hip_status(rb::launch_knn(p, queries, bank, bank_norms, ws, nbr, nbr_dist, bank_qual,
                                      bank_len, M, q_hat, l_hat,
-                                     o->weighting == RB_KNN_INV_DIST, (hipStream_t)stream));
+                                     o->weighting == RB_KNN_INV_DIST, (hipStream_t)stream,
+                                     phases));
 }
 
 rb_status rb_route_batch(const void *queries, const void *bank, const float *bank_norms,

@@ -83,12 +83,15 @@ void set_scan_events(hipEvent_t begin, hipEvent_t end);
 
 hipError_t launch_bank_norms(const void *bank, int dtype, int N, int d, float *norms,
                              hipStream_t s);
+// The halves of launch_knn: the seed and the bank scan (which leave the
+// per-chunk lists in the workspace), and the merge of those lists.
+enum KnnPhases { KNN_LISTS = 1, KNN_MERGE = 2, KNN_ALL = 3 };
 // With q_hat non-null, the merge also averages the labels (inv_dist: with
 // inverse-distance weights instead of the plain mean).
 hipError_t launch_knn(const KnnPlan &p, const void *queries, const void *bank,
                       const float *bank_norms, void *ws, int32_t *nbr_idx, float *nbr_dist,
                       const float *bank_qual, const float *bank_len, int M, float *q_hat,
-                      float *l_hat, bool inv_dist, hipStream_t s);
+                      float *l_hat, bool inv_dist, hipStream_t s, int phases = KNN_ALL);
 hipError_t launch_predict(const int32_t *nbr_idx, const float *nbr_dist, int B, int k,
                           bool inv_dist, const float *bank_qual, const float *bank_len, int N,
                           int M, float *q_hat, float *l_hat, hipStream_t s);

@@ -642,7 +642,7 @@ hipError_t launch_bank_norms(const void *bank, int dtype, int N, int d, float *n
 hipError_t launch_knn(const KnnPlan &p, const void *queries, const void *bank,
                       const float *bank_norms, void *ws, int32_t *nbr_idx, float *nbr_dist,
                       const float *bank_qual, const float *bank_len, int M, float *q_hat,
-                      float *l_hat, bool inv_dist, hipStream_t s)
+                      float *l_hat, bool inv_dist, hipStream_t s, int phases)
 {
     uint8_t *w = (uint8_t *)ws;
     uint32_t *tau = (uint32_t *)(w + p.off_tau);
@@ -653,75 +653,80 @@ hipError_t launch_knn(const KnnPlan &p, const void *queries, const void *bank,
     int32_t *cidx = (int32_t *)(w + p.off_cidx);
     hipError_t e;
 
-    if (p.S > 0) {
-        SeedArgs sa;
-        sa.queries = (const uint8_t *)queries;
-        sa.bank = (const uint8_t *)bank;
-        sa.bank_norms = bank_norms;
-        sa.B = p.B;
-        sa.N = p.N;
-        sa.d = p.d;
-        sa.nks = p.nks;
-        sa.S = p.S;
-        sa.G = p.G;
-        sa.n_qg = (p.B + 15) / 16;
-        sa.gmin = gmin;
-        // 16 query groups per workgroup, or 4 for a batch of at most 64
-        const int qg = sa.n_qg <= 4 ? 4 : 16;
-        const dim3 grid((p.G + SEED_WAVES - 1) / SEED_WAVES, (sa.n_qg + qg - 1) / qg);
-        const dim3 block(SEED_WAVES * WAVE);
-        if (p.dtype == 1) {
-            if (qg == 4)
-                hipLaunchKernelGGL((seed_groups_kernel<1, 4>), grid, block, 0, s, sa);
-            else
-                hipLaunchKernelGGL((seed_groups_kernel<1, 16>), grid, block, 0, s, sa);
-        } else {
-            if (qg == 4)
-                hipLaunchKernelGGL((seed_groups_kernel<0, 4>), grid, block, 0, s, sa);
-            else
-                hipLaunchKernelGGL((seed_groups_kernel<0, 16>), grid, block, 0, s, sa);
+    if (phases & KNN_LISTS) {
+        if (p.S > 0) {
+            SeedArgs sa;
+            sa.queries = (const uint8_t *)queries;
+            sa.bank = (const uint8_t *)bank;
+            sa.bank_norms = bank_norms;
+            sa.B = p.B;
+            sa.N = p.N;
+            sa.d = p.d;
+            sa.nks = p.nks;
+            sa.S = p.S;
+            sa.G = p.G;
+            sa.n_qg = (p.B + 15) / 16;
+            sa.gmin = gmin;
+            // 16 query groups per workgroup, or 4 for a batch of at most 64
+            const int qg = sa.n_qg <= 4 ? 4 : 16;
+            const dim3 grid((p.G + SEED_WAVES - 1) / SEED_WAVES, (sa.n_qg + qg - 1) / qg);
+            const dim3 block(SEED_WAVES * WAVE);
+            if (p.dtype == 1) {
+                if (qg == 4)
+                    hipLaunchKernelGGL((seed_groups_kernel<1, 4>), grid, block, 0, s, sa);
+                else
+                    hipLaunchKernelGGL((seed_groups_kernel<1, 16>), grid, block, 0, s, sa);
+            } else {
+                if (qg == 4)
+                    hipLaunchKernelGGL((seed_groups_kernel<0, 4>), grid, block, 0, s, sa);
+                else
+                    hipLaunchKernelGGL((seed_groups_kernel<0, 16>), grid, block, 0, s, sa);
+            }
+            if ((e = hipGetLastError()) != hipSuccess)
+                return e;
         }
-        if ((e = hipGetLastError()) != hipSuccess)
+        e = p.dtype == 1 ? launch_seed_bound<1>(p, queries, gmin, qn, tau, s)
+                         : launch_seed_bound<0>(p, queries, gmin, qn, tau, s);
+        if (e != hipSuccess)
+            return e;
+
+        ScanArgs a;
+        a.queries = (const uint8_t *)queries;
+        a.bank = (const uint8_t *)bank;
+        a.bank_norms = bank_norms;
+        a.qn = qn;
+        a.B = p.B;
+        a.N = p.N;
+        a.d = p.d;
+        a.k = p.k;
+        a.nks = p.nks;
+        a.nksp = p.nksp;
+        a.n_chunks = p.n_chunks;
+        a.n_qt = p.n_qt;
+        a.rows_per_chunk = p.rows_per_chunk;
+        a.tau = tau;
+        a.ccnt = ccnt;
+        a.ckey = ckey;
+        a.cidx = cidx;
+        a.ovf = (uint32_t *)(w + p.off_ovf);
+        a.ovf_cap = p.ovf_cap;
+        const bool timed = t_scan_begin && t_scan_end;
+        if (timed && (e = hipEventRecord(t_scan_begin, s)) != hipSuccess)
+            return e;
+        const bool ragged = p.d % (p.dtype == 1 ? 32 : 16) != 0;
+        if (p.kind == 1)
+            e = launch_scan_rq(p, a, s);
+        else
+            e = p.dtype == 1
+                    ? (ragged ? launch_scan_bf16_ragged(p, a, s) : launch_scan_bf16(p, a, s))
+                    : (ragged ? launch_scan_f32_ragged(p, a, s) : launch_scan_f32(p, a, s));
+        if (e != hipSuccess)
+            return e;
+        if (timed && (e = hipEventRecord(t_scan_end, s)) != hipSuccess)
             return e;
     }
-    e = p.dtype == 1 ? launch_seed_bound<1>(p, queries, gmin, qn, tau, s)
-                     : launch_seed_bound<0>(p, queries, gmin, qn, tau, s);
-    if (e != hipSuccess)
-        return e;
-
-    ScanArgs a;
-    a.queries = (const uint8_t *)queries;
-    a.bank = (const uint8_t *)bank;
-    a.bank_norms = bank_norms;
-    a.qn = qn;
-    a.B = p.B;
-    a.N = p.N;
-    a.d = p.d;
-    a.k = p.k;
-    a.nks = p.nks;
-    a.nksp = p.nksp;
-    a.n_chunks = p.n_chunks;
-    a.n_qt = p.n_qt;
-    a.rows_per_chunk = p.rows_per_chunk;
-    a.tau = tau;
-    a.ccnt = ccnt;
-    a.ckey = ckey;
-    a.cidx = cidx;
-    a.ovf = (uint32_t *)(w + p.off_ovf);
-    a.ovf_cap = p.ovf_cap;
-    const bool timed = t_scan_begin && t_scan_end;
-    if (timed && (e = hipEventRecord(t_scan_begin, s)) != hipSuccess)
-        return e;
-    const bool ragged = p.d % (p.dtype == 1 ? 32 : 16) != 0;
-    if (p.kind == 1)
-        e = launch_scan_rq(p, a, s);
-    else
-        e = p.dtype == 1 ? (ragged ? launch_scan_bf16_ragged(p, a, s) : launch_scan_bf16(p, a, s))
-                         : (ragged ? launch_scan_f32_ragged(p, a, s) : launch_scan_f32(p, a, s));
-    if (e != hipSuccess)
-        return e;
-    if (timed && (e = hipEventRecord(t_scan_end, s)) != hipSuccess)
-        return e;
+    if (!(phases & KNN_MERGE))
+        return hipSuccess;
 
     MergeArgs m;
     m.ccnt = ccnt;

@@ -180,6 +180,8 @@ def test_assign_ex_validation():
     assert call(rb.rb_options(2, 0, None, None, None)) == rb.RB_ERR_UNSUPPORTED
     assert call(rb.rb_options(0, 5, None, None, None)) == rb.RB_ERR_UNSUPPORTED
     assert call(rb.rb_options(-1, 0, None, None, None)) == rb.RB_ERR_UNSUPPORTED
+    assert call(rb.rb_options(0, 0, None, None, None, rb.RB_FLAG_FROM_LISTS)) == \
+        rb.RB_ERR_UNSUPPORTED   # a flag of rb_knn_predict only
     # LPT needs order_out
     assert call(rb.rb_options(rb.RB_ORDER_LPT, 0, None, None, None)) == rb.RB_ERR_NULL
     assert call(rb.rb_options(0, 0, None, None, None), asg=None) == rb.RB_ERR_NULL
@@ -202,6 +204,9 @@ def test_route_batch_ex_validation():
                                    None, None, None, None, FAKE, 1 << 20, None)
     assert call(rb.rb_options(3, 0, None, None, None)) == rb.RB_ERR_UNSUPPORTED
     assert call(rb.rb_options(0, 3, None, None, None)) == rb.RB_ERR_UNSUPPORTED
+    # the split-lookup flags belong to rb_knn_predict only
+    for f in (rb.RB_FLAG_LISTS_ONLY, rb.RB_FLAG_FROM_LISTS):
+        assert call(rb.rb_options(0, 0, None, None, None, f)) == rb.RB_ERR_UNSUPPORTED
     assert call(None, asg=None) == rb.RB_ERR_NULL
     assert call(None, q=MISALIGNED) == rb.RB_ERR_ALIGN
     assert call(rb.rb_options(rb.RB_ORDER_LPT, rb.RB_KNN_INV_DIST, None, None, None), B=0, q=None,
@@ -223,9 +228,21 @@ def test_knn_predict_validation():
     assert call(qual=None) == rb.RB_ERR_NULL
     assert call(q=MISALIGNED) == rb.RB_ERR_ALIGN
     assert call(rb.rb_options(0, 2, None, None, None, 0)) == rb.RB_ERR_UNSUPPORTED
-    assert call(rb.rb_options(0, 0, None, None, None, 2)) == rb.RB_ERR_UNSUPPORTED   # unknown flag
+    assert call(rb.rb_options(0, 0, None, None, None, 8)) == rb.RB_ERR_UNSUPPORTED   # unknown flag
     assert call(rb.rb_options(0, 0, None, None, None, rb.RB_FLAG_OVERLAP), B=0, q=None, qh=None,
                 lh=None, ws=None) == rb.RB_OK
+    # the split lookup: not both halves at once; the scan half needs no outputs,
+    # the merge half no queries (both then stop at the device query or, with a
+    # device, at the missing workspace: nothing is launched)
+    both = rb.RB_FLAG_LISTS_ONLY | rb.RB_FLAG_FROM_LISTS
+    assert call(rb.rb_options(0, 0, None, None, None, both)) == rb.RB_ERR_UNSUPPORTED
+    lists = rb.rb_options(0, 0, None, None, None, rb.RB_FLAG_LISTS_ONLY)
+    merge = rb.rb_options(0, 0, None, None, None, rb.RB_FLAG_FROM_LISTS)
+    assert call(lists, q=None) == rb.RB_ERR_NULL
+    assert call(merge, qh=None) == rb.RB_ERR_NULL
+    assert call(lists, qh=None, lh=None, qual=None, ws=None) in (rb.RB_ERR_HIP,
+                                                                 rb.RB_ERR_WORKSPACE)
+    assert call(merge, q=None, ws=None) in (rb.RB_ERR_HIP, rb.RB_ERR_WORKSPACE)
 
 
 def test_struct_layouts_match_the_header(tmp_path):

@@ -47,6 +47,26 @@ def test_knn_predict_overlap_flag_changes_nothing(name, over):
             torch.cuda.synchronize()
             outs.append((flags, wt, idx.cpu().numpy(), dist.cpu().numpy(), qh.cpu().numpy(),
                          lh.cpu().numpy()))
+            # the same lookup in two calls on two streams: the scan half, an
+            # event, the merge half
+            s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+            ws = rb.workspace(cfg.B, cfg.N, cfg.d, rb._dtype_code(c["bank"]), cfg.k, cfg.M, DEV)
+            ev = torch.cuda.Event()
+            torch.cuda.synchronize()
+            rb.rb_knn_predict(q, c["bank"], c["norms"], cfg.k, c["gq"], c["gl"],
+                              rb.options(weighting=wt, flags=flags | rb.RB_FLAG_LISTS_ONLY),
+                              ws=ws, stream=s1)
+            ev.record(s1)
+            s2.wait_event(ev)
+            idx = torch.empty(cfg.B, cfg.k, dtype=torch.int32, device=DEV)
+            dist = torch.empty(cfg.B, cfg.k, device=DEV)
+            qh, lh = rb.rb_knn_predict(q, c["bank"], c["norms"], cfg.k, c["gq"], c["gl"],
+                                       rb.options(weighting=wt,
+                                                  flags=flags | rb.RB_FLAG_FROM_LISTS),
+                                       ws=ws, nbr_idx=idx, nbr_dist=dist, stream=s2)
+            torch.cuda.synchronize()
+            outs.append((flags, wt, idx.cpu().numpy(), dist.cpu().numpy(), qh.cpu().numpy(),
+                         lh.cpu().numpy()))
     # the fused route call's own lists and predictions
     gi = rb.DeviceInstances.from_host(c["inst_h"], DEV)
     idx = torch.empty(cfg.B, cfg.k, dtype=torch.int32, device=DEV)
@@ -66,10 +86,13 @@ def test_knn_predict_overlap_flag_changes_nothing(name, over):
             assert np.array_equal(b.view(np.uint32), lh.cpu().numpy().view(np.uint32))
 
 
-@pytest.mark.parametrize("name,batches", [("online", 5), ("highload", 4)])
-def test_pipelined_schedule_matches_sequential(name, batches):
+@pytest.mark.parametrize("name,batches,split", [("online", 5, False), ("highload", 4, False),
+                                                ("online", 5, True), ("highload", 4, True)])
+def test_pipelined_schedule_matches_sequential(name, batches, split):
+    """split: the scan half of every lookup on one stream, the merge half with
+    the greedy pass on the other, each batch with its own workspace."""
     cfg = synth.CONFIGS[name]
-    say(f"pipeline {name}: B={cfg.B} N={cfg.N}, {batches} carried batches")
+    say(f"pipeline {name}: B={cfg.B} N={cfg.N}, {batches} carried batches, split={split}")
     c = setup(cfg)
     rb = c["rb"]
     qs = [synth.make_queries(cfg, t, DEV, c["centres"]) for t in range(batches)]
@@ -107,11 +130,25 @@ def test_pipelined_schedule_matches_sequential(name, batches):
                           q_hat=qh[t % 2], l_hat=lh[t % 2], stream=s_knn)
         ev_k[t].record(s_knn)
 
+    if split:
+        wss = [rb.workspace(cfg.B, cfg.N, cfg.d, rb.RB_BF16, cfg.k, cfg.M, DEV)
+               for _ in range(batches)]
+        lopt = rb.options(flags=rb.RB_FLAG_OVERLAP | rb.RB_FLAG_LISTS_ONLY)
+        mopt = rb.options(flags=rb.RB_FLAG_OVERLAP | rb.RB_FLAG_FROM_LISTS)
+
+        def lookup(t):
+            rb.rb_knn_predict(qs[t], c["bank"], c["norms"], cfg.k, c["gq"], c["gl"], lopt,
+                              ws=wss[t], stream=s_knn)
+            ev_k[t].record(s_knn)
+
     lookup(0)
     for t in range(batches):
         if t + 1 < batches:
             lookup(t + 1)
         s_asg.wait_event(ev_k[t])
+        if split:
+            rb.rb_knn_predict(qs[t], c["bank"], c["norms"], cfg.k, c["gq"], c["gl"], mopt,
+                              ws=wss[t], q_hat=qh[t % 2], l_hat=lh[t % 2], stream=s_asg)
         a, _ = rb.rb_assign_ex(qh[t % 2], lh[t % 2], pls[t], gi, cfg.weights, aopt,
                                stream=s_asg, want_chosen=False)
         rb.rb_advance_state(gi, dt, stream=s_asg)
