@@ -312,11 +312,13 @@ rb_status rb_route_batch_ex(const void *queries, const void *bank, const float *
  * RB_ERR_HIP. */
 rb_status rb_advance_state(const rb_instances *inst, int I, float dt_seconds, void *stream);
 
-/* Timing hook for the bank scan, the dominant kernel of rb_knn_topk and
- * rb_route_batch. While set, every later call of those two entry points made
- * from the calling host thread records `begin` (a hipEvent_t) on the call's
- * stream immediately before the bank-scan kernel and `end` immediately after
- * it, so hipEventElapsedTime(begin, end) is that kernel's duration. Pass NULL,
+/* Timing hook for the bank scan, the dominant kernel of rb_knn_topk,
+ * rb_knn_predict and the rb_route_batch calls. While set, every later call of
+ * those entry points that runs the scan (not rb_knn_predict with
+ * RB_FLAG_FROM_LISTS) made from the calling host thread records `begin` (a
+ * hipEvent_t) on the call's stream immediately before the bank-scan kernel and
+ * `end` immediately after it, so hipEventElapsedTime(begin, end) is that
+ * kernel's duration. Pass NULL,
  * NULL to stop. The setting is per host thread; the events stay owned by the
  * caller. Always returns RB_OK. */
 rb_status rb_profile_scan_events(void *begin, void *end);
