@@ -29,10 +29,10 @@
  *     an availability mask every instance is a candidate; a zero maximum makes
  *     that ratio 0;
  *   - candidate set (Alg. 1 budget filter, Eq. 2): an instance is a candidate
- *     when it is available and its expected cost is at most the request's
- *     budget; the admission test is taken in fp32, fma(l_r, c_in, L*c_out) <=
- *     b_r, the precision the GPU path decides it in; a request with no
- *     candidate is left unassigned (-1) and changes no state;
+ *     when it is available and its expected cost l_r*c_in + L*c_out, taken
+ *     in fp64 like every other value here, is at most the request's budget
+ *     b_r; a request with no candidate is left unassigned (-1) and changes no
+ *     state;
  *   - argmax ties go to the lowest instance index;
  *   - processing order: arrival order (batch index order) by default; the LPT
  *     option (Alg. 1, Sec. 4.1) sorts by max over models of L[r][m], longest
@@ -219,18 +219,19 @@ typedef struct {
 
 /* Candidate set of one request (Alg. 1 budget filter; Eq. 2): instance i is
  * a candidate when mask is NULL or mask[i] != 0, and budget_r is NULL or the
- * expected cost fits it. The cost for this test is computed in fp32 as
- * fma(l_r, c_in, L*c_out), the precision and rounding the GPU path decides
- * it in, so both sides admit the same instances. Writes cand[I] (0/1). */
+ * expected cost of Eq. 2, input tokens at the input price plus predicted
+ * output tokens at the output price, is at most the budget. The cost is the
+ * same fp64 value the score uses (for fp32 inputs the two products are exact
+ * and the sum is rounded once), compared with the budget widened exactly.
+ * A NaN budget admits nothing. Writes cand[I] (0/1). */
 static void candidates(const double *l_hat_r, double plen, const orc_inst *in, int I,
                        const float *budget_r, const uint8_t *mask, unsigned char *cand)
 {
     for (int i = 0; i < I; ++i) {
         int ok = mask ? mask[i] != 0 : 1;
         if (ok && budget_r) {
-            float lv = (float)l_hat_r[in->model[i]];
-            float c = fmaf((float)plen, (float)in->cin[i], lv * (float)in->cout[i]);
-            ok = c <= *budget_r;
+            double c = plen * in->cin[i] + l_hat_r[in->model[i]] * in->cout[i];
+            ok = c <= (double)*budget_r;
         }
         cand[i] = (unsigned char)ok;
     }

@@ -51,7 +51,15 @@ MUTANTS = [
      "return 1.0 / (fmax(d, 0.0) + 1e-6);"),
     ("negative distance not clamped", "sqrt(fmax(d, 0.0))", "sqrt(fabs(d))"),
     ("weights not normalised", "sw += wj;", "sw += 1.0;"),
-    ("budget admits strictly below only", "ok = c <= *budget_r;", "ok = c < *budget_r;"),
+    ("budget admits strictly below only", "ok = c <= (double)*budget_r;",
+     "ok = c < (double)*budget_r;"),
+    ("budget admission in fp32 rounding",
+     "double c = plen * in->cin[i] + l_hat_r[in->model[i]] * in->cout[i];",
+     "double c = fmaf((float)plen, (float)in->cin[i],\n"
+     "                            (float)l_hat_r[in->model[i]] * (float)in->cout[i]);"),
+    ("budget compared with the output cost only",
+     "double c = plen * in->cin[i] + l_hat_r[in->model[i]] * in->cout[i];",
+     "double c = l_hat_r[in->model[i]] * in->cout[i];"),
     ("mask ignored", "int ok = mask ? mask[i] != 0 : 1;", "int ok = 1;"),
     ("maxima over every instance",
      "        if (cand && !cand[i])\n            continue;\n        if (!seen || C[i] > cmax)",

@@ -466,6 +466,62 @@ def test_budget_and_mask_hand_examples():
         assert r["assign"].tolist() == [admitted[0] if admitted else -1]
 
 
+def _exact_cost(l, cin, L, cout):
+    """Eq. 2 cost of fp32 inputs in exact rational arithmetic."""
+    from fractions import Fraction as F
+    return F(int(l)) * F(float(cin)) + F(float(L)) * F(float(cout))
+
+
+def _fp32_cost(l, cin, L, cout):
+    """The same cost in fp32 with one fused multiply-add (C library fmaf)."""
+    import ctypes
+    import ctypes.util
+    libm = ctypes.CDLL(ctypes.util.find_library("m"))
+    libm.fmaf.restype = ctypes.c_float
+    libm.fmaf.argtypes = [ctypes.c_float] * 3
+    return np.float32(libm.fmaf(float(np.float32(l)), float(cin),
+                                float(np.float32(np.float32(L) * np.float32(cout)))))
+
+
+def test_budget_admission_is_exact_at_one_ulp():
+    # Eq. 2 compares the expected cost with the budget; the oracle decides it
+    # on the exact cost. Find fp32 inputs whose exact cost lies strictly
+    # between two adjacent fp32 budgets b_lo < C < b_hi while the fp32 fused
+    # evaluation rounds to b_lo: b_lo must reject (although fp32 arithmetic
+    # would admit), b_hi must admit, and a budget equal to an exactly
+    # representable cost admits (the boundary case of the hand example).
+    from fractions import Fraction as F
+    rng = np.random.default_rng(17)
+    found = 0
+    for _ in range(2000):
+        l = int(rng.integers(50, 5000))
+        L = np.float32(rng.integers(1, 2000))
+        cin = np.float32(rng.uniform(1e-4, 2e-3))
+        cout = np.float32(rng.uniform(1e-4, 2e-3))
+        C = _exact_cost(l, cin, L, cout)
+        lo = np.float32(float(C))
+        if F(float(lo)) > C:
+            lo = np.nextafter(lo, np.float32(-np.inf))
+        hi = np.nextafter(lo, np.float32(np.inf))
+        if not F(float(lo)) < C < F(float(hi)) or _fp32_cost(l, cin, L, cout) > lo:
+            continue
+        inst = synth.Instances(np.array([0], np.int32), np.zeros(1, np.float32),
+                               np.zeros(1, np.float32), np.full(1, 1e4, np.float32),
+                               np.full(1, 1e3, np.float32), np.array([cin]), np.array([cout]))
+        for budget, admit in ((lo, False), (hi, True)):
+            _, _, Cc, cand = oracle.score_row([0.5], [float(L)], l, inst, np.zeros(1),
+                                              np.zeros(1), (0.4, 0.3, 0.3), budget_r=budget,
+                                              with_candidates=True)
+            assert bool(cand[0]) == admit, (l, float(L), float(cin), float(cout), float(budget))
+            r = oracle.assign(np.array([[0.5]]), np.array([[float(L)]]), np.array([l], np.int32),
+                              inst, (0.4, 0.3, 0.3), budget=np.array([budget], np.float32))
+            assert r["assign"].tolist() == [0 if admit else -1]
+        found += 1
+        if found == 20:
+            break
+    assert found == 20
+
+
 @pytest.mark.parametrize("seed", range(4))
 def test_mask_is_removing_instances(seed):
     # an unavailable instance is as if it were not in the table: the masked
