@@ -185,11 +185,16 @@ rb_status rb_score(const float *q_hat, const float *l_hat, const int32_t *prompt
  *   prefill_q[i*] += l_r;  decode_q[i*] += L[r][m(i*)].
  * Rates and prices are unchanged. Runs on one wavefront, fp32.
  *   assign [B] int32 (output); chosen_score [B] fp32 (output, may be NULL);
+ *   decided [B][I] fp32 (output, may be NULL): row r holds the Eq. 1 scores
+ *   of request r against every instance at the state it was decided in (the
+ *   logged score matrices Sec. 4.1 compares the greedy pass with), NaN for
+ *   an instance outside its candidate set; chosen_score[r] equals
+ *   decided[r][assign[r]] bit for bit. Writing it slows the loop.
  *   inst->prefill_q / decode_q are updated in place.
  * Errors: as rb_score, plus RB_ERR_NULL for assign. */
 rb_status rb_assign(const float *q_hat, const float *l_hat, const int32_t *prompt_len, int B,
                     int M, const rb_instances *inst, int I, rb_weights w, int32_t *assign,
-                    float *chosen_score, void *stream);
+                    float *chosen_score, float *decided, void *stream);
 
 /* Flags of rb_options.
  *   RB_FLAG_OVERLAP: the bank scan of rb_knn_predict / rb_route_batch_ex
@@ -249,27 +254,31 @@ typedef struct {
 } rb_options;
 
 /* rb_assign with options (Alg. 1 with its LPT order and budget filter, and an
- * instance availability mask). assign [B] and chosen_score [B] stay indexed by
- * request whatever the order. Errors: as rb_assign, plus RB_ERR_UNSUPPORTED
- * (order or weighting out of range), RB_ERR_NULL (order_out missing for
- * RB_ORDER_LPT). */
+ * instance availability mask). assign [B], chosen_score [B] and the rows of
+ * decided [B][I] (may be NULL) stay indexed by request whatever the order.
+ * Errors: as rb_assign, plus RB_ERR_UNSUPPORTED (order or weighting out of
+ * range), RB_ERR_NULL (order_out missing for RB_ORDER_LPT). */
 rb_status rb_assign_ex(const float *q_hat, const float *l_hat, const int32_t *prompt_len, int B,
                        int M, const rb_instances *inst, int I, rb_weights w,
                        const rb_options *opts, int32_t *assign, float *chosen_score,
-                       void *stream);
+                       float *decided, void *stream);
 
-/* The whole path for one batch: rb_knn_topk, then rb_predict (uniform), then
- * rb_assign, enqueued back to back on `stream`. The intermediate outputs
- * nbr_idx [B][k], nbr_dist [B][k], q_hat [B][M], l_hat [B][M] and
- * chosen_score [B] are written when their pointers are non-NULL and otherwise
- * kept in the workspace. inst state is updated in place as by rb_assign.
+/* The whole path for one batch (Alg. 1: one batched KNN lookup, the
+ * predictions of Sec. 4.2, then the greedy loop): rb_knn_topk, then
+ * rb_predict (uniform), then rb_assign, enqueued back to back on `stream`.
+ * The intermediate outputs nbr_idx [B][k], nbr_dist [B][k], q_hat [B][M],
+ * l_hat [B][M] and chosen_score [B] are written when their pointers are
+ * non-NULL and otherwise kept in the workspace. score0 [B][I] (may be NULL)
+ * receives the dense Eq. 1 matrix at the batch-start state, as rb_score
+ * computes it, before the greedy loop changes the state. inst state is
+ * updated in place as by rb_assign.
  * Errors: the union of those of the three calls. */
 rb_status rb_route_batch(const void *queries, const void *bank, const float *bank_norms,
                          rb_dtype dtype, int B, int N, int d, int k, const float *bank_qual,
                          const float *bank_len, int M, const int32_t *prompt_len,
                          const rb_instances *inst, int I, rb_weights w, int32_t *assign,
                          float *chosen_score, int32_t *nbr_idx, float *nbr_dist, float *q_hat,
-                         float *l_hat, void *ws, size_t ws_bytes, void *stream);
+                         float *l_hat, float *score0, void *ws, size_t ws_bytes, void *stream);
 
 /* The estimation half of the path for one batch (Alg. 1's one batched KNN
  * lookup): rb_knn_topk, then the label average of opts->weighting, in one
@@ -293,7 +302,9 @@ rb_status rb_knn_predict(const void *queries, const void *bank, const float *ban
                          void *stream);
 
 /* rb_route_batch with options: the averaging rule of opts->weighting, then
- * rb_assign_ex's order, budgets and mask. The workspace is the same size as
+ * rb_assign_ex's order, budgets and mask. score0 (may be NULL) then holds
+ * each request's row over its candidate set (the maxima over the candidates,
+ * NaN elsewhere), at the batch-start state. The workspace is the same size as
  * for rb_route_batch (rb_workspace_size). Errors: the union of those of
  * rb_route_batch and rb_assign_ex (order_out is optional here). */
 rb_status rb_route_batch_ex(const void *queries, const void *bank, const float *bank_norms,
@@ -302,7 +313,7 @@ rb_status rb_route_batch_ex(const void *queries, const void *bank, const float *
                             const rb_instances *inst, int I, rb_weights w,
                             const rb_options *opts, int32_t *assign, float *chosen_score,
                             int32_t *nbr_idx, float *nbr_dist, float *q_hat, float *l_hat,
-                            void *ws, size_t ws_bytes, void *stream);
+                            float *score0, void *ws, size_t ws_bytes, void *stream);
 
 /* Carry the dead-reckoned state across a gap of dt_seconds between batches:
  *   prefill_q[i] = max(0, prefill_q[i] - prefill_rate[i]*dt)

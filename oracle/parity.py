@@ -274,6 +274,21 @@ def check_assign(g_assign, g_chosen, g_qhat, g_lhat, plen, inst, weights, g_fina
     return counts["pick"] + counts["admission"]
 
 
+def replay_state(g_assign, g_lhat, plen, inst, p0, a0):
+    """The state after a batch's picks (the dead-reckoning update of Sec. 4.2,
+    p += l_r and a += L[r][m(i)] for each assigned request), in fp64 from
+    (p0, a0). Unassigned requests (-1) change nothing."""
+    p = np.asarray(p0, np.float64).copy()
+    a = np.asarray(a0, np.float64).copy()
+    lh = np.asarray(g_lhat, np.float64)
+    model = np.asarray(inst.model)
+    for r, i in enumerate(np.asarray(g_assign).tolist()):
+        if i >= 0:
+            p[i] += plen[r]
+            a[i] += lh[r, model[i]]
+    return p, a
+
+
 def free_running(queries, bank, k, qual, length, plen, inst, weights, nthreads=1,
                  order="arrival", weighting="uniform", budget=None, mask=None):
     """The oracle alone: its own KNN, predictions and greedy loop."""

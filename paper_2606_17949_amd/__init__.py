@@ -70,16 +70,17 @@ def _load():
         "rb_knn_topk": ([P, P, P, i, i, i, i, i, P, P, P, sz, P], st),
         "rb_predict": ([P, P, i, i, i, P, P, i, i, P, P, P], st),
         "rb_score": ([P, P, P, i, i, ctypes.POINTER(rb_instances), i, rb_weights, P, P], st),
-        "rb_assign": ([P, P, P, i, i, ctypes.POINTER(rb_instances), i, rb_weights, P, P, P], st),
+        "rb_assign": ([P, P, P, i, i, ctypes.POINTER(rb_instances), i, rb_weights, P, P, P, P],
+                      st),
         "rb_assign_ex": ([P, P, P, i, i, ctypes.POINTER(rb_instances), i, rb_weights,
-                          ctypes.POINTER(rb_options), P, P, P], st),
+                          ctypes.POINTER(rb_options), P, P, P, P], st),
         "rb_knn_predict": ([P, P, P, i, i, i, i, i, P, P, i, ctypes.POINTER(rb_options), P, P, P,
                             P, P, sz, P], st),
         "rb_route_batch": ([P, P, P, i, i, i, i, i, P, P, i, P, ctypes.POINTER(rb_instances), i,
-                            rb_weights, P, P, P, P, P, P, P, sz, P], st),
+                            rb_weights, P, P, P, P, P, P, P, P, sz, P], st),
         "rb_route_batch_ex": ([P, P, P, i, i, i, i, i, P, P, i, P, ctypes.POINTER(rb_instances),
-                               i, rb_weights, ctypes.POINTER(rb_options), P, P, P, P, P, P, P, sz,
-                               P], st),
+                               i, rb_weights, ctypes.POINTER(rb_options), P, P, P, P, P, P, P, P,
+                               sz, P], st),
         "rb_advance_state": ([ctypes.POINTER(rb_instances), i, ctypes.c_float, P], st),
         "rb_profile_scan_events": ([P, P], st),
     }
@@ -126,10 +127,55 @@ def _dtype_code(t: torch.Tensor) -> int:
 
 
 def _expect(t: torch.Tensor, dtype, shape, name):
+    """dtype and shape of a tensor argument, checked before anything reaches
+    the library (a short or mistyped buffer would be read or written out of
+    bounds on the GPU)."""
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name}: expected a torch tensor, got {type(t).__name__}")
     if t.dtype != dtype:
         raise ValueError(f"{name}: expected {dtype}, got {t.dtype}")
     if tuple(t.shape) != tuple(shape):
         raise ValueError(f"{name}: expected shape {tuple(shape)}, got {tuple(t.shape)}")
+
+
+def _expect_opt(t: Optional[torch.Tensor], dtype, shape, name):
+    if t is not None:
+        _expect(t, dtype, shape, name)
+
+
+def _embeddings(queries, bank):
+    """(B, N, d) of a query batch and a bank of the same dtype and width."""
+    for t, name in ((queries, "queries"), (bank, "bank")):
+        if not isinstance(t, torch.Tensor) or t.dim() != 2:
+            raise ValueError(f"{name}: expected a 2-d tensor")
+        if t.dtype not in (torch.float32, torch.bfloat16):
+            raise ValueError(f"{name}: unsupported embedding dtype {t.dtype}")
+    if queries.dtype != bank.dtype:
+        raise ValueError(f"queries ({queries.dtype}) and bank ({bank.dtype}) must share a dtype")
+    if queries.shape[1] != bank.shape[1]:
+        raise ValueError(f"queries (d={queries.shape[1]}) and bank (d={bank.shape[1]}) must "
+                         "share the embedding width")
+    return int(queries.shape[0]), int(bank.shape[0]), int(bank.shape[1])
+
+
+def _labels(bank_qual, bank_len, N):
+    """M of the per-model label tables [N][M] fp32."""
+    if not isinstance(bank_qual, torch.Tensor) or bank_qual.dim() != 2:
+        raise ValueError("bank_qual: expected a 2-d tensor")
+    M = int(bank_qual.shape[1])
+    _expect(bank_qual, torch.float32, (N, M), "bank_qual")
+    _expect(bank_len, torch.float32, (N, M), "bank_len")
+    return M
+
+
+def _predictions(q_hat, l_hat):
+    """(B, M) of the prediction tables [B][M] fp32."""
+    if not isinstance(q_hat, torch.Tensor) or q_hat.dim() != 2:
+        raise ValueError("q_hat: expected a 2-d tensor")
+    B, M = (int(x) for x in q_hat.shape)
+    _expect(q_hat, torch.float32, (B, M), "q_hat")
+    _expect(l_hat, torch.float32, (B, M), "l_hat")
+    return B, M
 
 
 @dataclasses.dataclass
@@ -188,6 +234,9 @@ def workspace(B: int, N: int, d: int, dtype: int, k: int, M: int, device="cuda")
 
 
 def rb_bank_norms(bank: torch.Tensor, norms: Optional[torch.Tensor] = None, stream=None):
+    if not isinstance(bank, torch.Tensor) or bank.dim() != 2 or \
+            bank.dtype not in (torch.float32, torch.bfloat16):
+        raise ValueError("bank: expected a 2-d fp32 or bf16 tensor")
     N, d = bank.shape
     if norms is None:
         norms = torch.empty(N, dtype=torch.float32, device=bank.device)
@@ -200,10 +249,11 @@ def rb_bank_norms(bank: torch.Tensor, norms: Optional[torch.Tensor] = None, stre
 def rb_knn_topk(queries: torch.Tensor, bank: torch.Tensor, bank_norms: torch.Tensor, k: int,
                 nbr_idx: Optional[torch.Tensor] = None, nbr_dist: Optional[torch.Tensor] = None,
                 ws: Optional[torch.Tensor] = None, stream=None, want_dist: bool = True):
-    B, d = queries.shape
-    N, d2 = bank.shape
-    if d != d2 or queries.dtype != bank.dtype:
-        raise ValueError("queries and bank must share dtype and dimension")
+    B, N, d = _embeddings(queries, bank)
+    _expect(bank_norms, torch.float32, (N,), "bank_norms")
+    _expect_opt(nbr_idx, torch.int32, (B, k), "nbr_idx")
+    _expect_opt(nbr_dist, torch.float32, (B, k), "nbr_dist")
+    _expect_opt(ws, torch.uint8, (ws.numel(),) if ws is not None else (), "ws")
     dev = queries.device
     if nbr_idx is None:
         nbr_idx = torch.empty(B, k, dtype=torch.int32, device=dev)
@@ -211,7 +261,6 @@ def rb_knn_topk(queries: torch.Tensor, bank: torch.Tensor, bank_norms: torch.Ten
         nbr_dist = torch.empty(B, k, dtype=torch.float32, device=dev)
     if ws is None:
         ws = workspace(B, N, d, _dtype_code(bank), k, 1, dev)
-    _expect(bank_norms, torch.float32, (N,), "bank_norms")
     _check(_lib.rb_knn_topk(_ptr(queries), _ptr(bank), _ptr(bank_norms), _dtype_code(bank), B, N,
                             d, k, _ptr(nbr_idx), _ptr(nbr_dist), _ptr(ws), ws.numel(),
                             _stream(stream)), "rb_knn_topk")
@@ -222,8 +271,17 @@ def rb_predict(nbr_idx: torch.Tensor, bank_qual: torch.Tensor, bank_len: torch.T
                nbr_dist: Optional[torch.Tensor] = None, weighting: int = RB_KNN_UNIFORM,
                q_hat: Optional[torch.Tensor] = None, l_hat: Optional[torch.Tensor] = None,
                stream=None):
-    B, k = nbr_idx.shape
-    N, M = bank_qual.shape
+    if not isinstance(nbr_idx, torch.Tensor) or nbr_idx.dim() != 2:
+        raise ValueError("nbr_idx: expected a 2-d tensor")
+    B, k = (int(x) for x in nbr_idx.shape)
+    _expect(nbr_idx, torch.int32, (B, k), "nbr_idx")
+    if not isinstance(bank_qual, torch.Tensor) or bank_qual.dim() != 2:
+        raise ValueError("bank_qual: expected a 2-d tensor")
+    N = int(bank_qual.shape[0])
+    M = _labels(bank_qual, bank_len, N)
+    _expect_opt(nbr_dist, torch.float32, (B, k), "nbr_dist")
+    _expect_opt(q_hat, torch.float32, (B, M), "q_hat")
+    _expect_opt(l_hat, torch.float32, (B, M), "l_hat")
     dev = nbr_idx.device
     if q_hat is None:
         q_hat = torch.empty(B, M, dtype=torch.float32, device=dev)
@@ -239,10 +297,17 @@ def _w(weights) -> rb_weights:
     return rb_weights(*[float(x) for x in weights])
 
 
+def _request_args(q_hat, l_hat, prompt_len):
+    B, M = _predictions(q_hat, l_hat)
+    _expect(prompt_len, torch.int32, (B,), "prompt_len")
+    return B, M
+
+
 def rb_score(q_hat, l_hat, prompt_len, inst: DeviceInstances, weights,
              score0: Optional[torch.Tensor] = None, stream=None):
-    B, M = q_hat.shape
+    B, M = _request_args(q_hat, l_hat, prompt_len)
     I = inst.I
+    _expect_opt(score0, torch.float32, (B, I), "score0")
     if score0 is None:
         score0 = torch.empty(B, I, dtype=torch.float32, device=q_hat.device)
     s = inst.struct()
@@ -251,20 +316,47 @@ def rb_score(q_hat, l_hat, prompt_len, inst: DeviceInstances, weights,
     return score0
 
 
-def rb_assign(q_hat, l_hat, prompt_len, inst: DeviceInstances, weights,
-              assign: Optional[torch.Tensor] = None, chosen: Optional[torch.Tensor] = None,
-              stream=None, want_chosen: bool = True):
-    B, M = q_hat.shape
-    dev = q_hat.device
+def _assign_outputs(B, I, dev, assign, chosen, decided, want_chosen):
+    _expect_opt(assign, torch.int32, (B,), "assign")
+    _expect_opt(chosen, torch.float32, (B,), "chosen")
+    _expect_opt(decided, torch.float32, (B, I), "decided")
     if assign is None:
         assign = torch.empty(B, dtype=torch.int32, device=dev)
     if chosen is None and want_chosen:
         chosen = torch.empty(B, dtype=torch.float32, device=dev)
+    return assign, chosen
+
+
+def rb_assign(q_hat, l_hat, prompt_len, inst: DeviceInstances, weights,
+              assign: Optional[torch.Tensor] = None, chosen: Optional[torch.Tensor] = None,
+              stream=None, want_chosen: bool = True, decided: Optional[torch.Tensor] = None):
+    """Greedy assignment; ``decided`` [B][I] fp32, when given, receives the
+    Eq. 1 row each request was decided on."""
+    B, M = _request_args(q_hat, l_hat, prompt_len)
+    assign, chosen = _assign_outputs(B, inst.I, q_hat.device, assign, chosen, decided,
+                                     want_chosen)
     s = inst.struct()
     _check(_lib.rb_assign(_ptr(q_hat), _ptr(l_hat), _ptr(prompt_len), B, M, ctypes.byref(s),
-                          inst.I, _w(weights), _ptr(assign), _ptr(chosen), _stream(stream)),
-           "rb_assign")
+                          inst.I, _w(weights), _ptr(assign), _ptr(chosen), _ptr(decided),
+                          _stream(stream)), "rb_assign")
     return assign, chosen
+
+
+def _route_args(queries, bank, bank_norms, k, bank_qual, bank_len, prompt_len, inst, ws,
+                nbr_idx, nbr_dist, q_hat, l_hat, score0, chosen, assign):
+    B, N, d = _embeddings(queries, bank)
+    _expect(bank_norms, torch.float32, (N,), "bank_norms")
+    M = _labels(bank_qual, bank_len, N)
+    _expect(prompt_len, torch.int32, (B,), "prompt_len")
+    _expect_opt(nbr_idx, torch.int32, (B, k), "nbr_idx")
+    _expect_opt(nbr_dist, torch.float32, (B, k), "nbr_dist")
+    _expect_opt(q_hat, torch.float32, (B, M), "q_hat")
+    _expect_opt(l_hat, torch.float32, (B, M), "l_hat")
+    _expect_opt(score0, torch.float32, (B, inst.I), "score0")
+    _expect_opt(chosen, torch.float32, (B,), "chosen")
+    _expect_opt(assign, torch.int32, (B,), "assign")
+    _expect_opt(ws, torch.uint8, (ws.numel(),) if ws is not None else (), "ws")
+    return B, N, d, M
 
 
 def rb_route_batch(queries, bank, bank_norms, k: int, bank_qual, bank_len, prompt_len,
@@ -272,11 +364,10 @@ def rb_route_batch(queries, bank, bank_norms, k: int, bank_qual, bank_len, promp
                    assign: Optional[torch.Tensor] = None, chosen: Optional[torch.Tensor] = None,
                    nbr_idx: Optional[torch.Tensor] = None, nbr_dist: Optional[torch.Tensor] = None,
                    q_hat: Optional[torch.Tensor] = None, l_hat: Optional[torch.Tensor] = None,
-                   stream=None):
+                   stream=None, score0: Optional[torch.Tensor] = None):
     """The fused path; intermediates are returned only if the caller passes buffers."""
-    B, d = queries.shape
-    N = bank.shape[0]
-    M = bank_qual.shape[1]
+    B, N, d, M = _route_args(queries, bank, bank_norms, k, bank_qual, bank_len, prompt_len, inst,
+                             ws, nbr_idx, nbr_dist, q_hat, l_hat, score0, chosen, assign)
     dev = queries.device
     if assign is None:
         assign = torch.empty(B, dtype=torch.int32, device=dev)
@@ -286,8 +377,9 @@ def rb_route_batch(queries, bank, bank_norms, k: int, bank_qual, bank_len, promp
     _check(_lib.rb_route_batch(_ptr(queries), _ptr(bank), _ptr(bank_norms), _dtype_code(bank), B,
                                N, d, k, _ptr(bank_qual), _ptr(bank_len), M, _ptr(prompt_len),
                                ctypes.byref(s), inst.I, _w(weights), _ptr(assign), _ptr(chosen),
-                               _ptr(nbr_idx), _ptr(nbr_dist), _ptr(q_hat), _ptr(l_hat), _ptr(ws),
-                               ws.numel(), _stream(stream)), "rb_route_batch")
+                               _ptr(nbr_idx), _ptr(nbr_dist), _ptr(q_hat), _ptr(l_hat),
+                               _ptr(score0), _ptr(ws), ws.numel(), _stream(stream)),
+           "rb_route_batch")
     return assign
 
 
@@ -303,6 +395,8 @@ def options(order: int = RB_ORDER_ARRIVAL, weighting: int = RB_KNN_UNIFORM,
                         (order_out, torch.int32, "order_out")):
         if t is not None and t.dtype != dt:
             raise ValueError(f"{name}: expected {dt}, got {t.dtype}")
+        if t is not None and not t.is_cuda:
+            raise ValueError(f"{name}: must live on the GPU")
     o = rb_options(int(order), int(weighting), _ptr(budget), _ptr(instance_mask),
                    _ptr(order_out), int(flags))
     o._tensors = (budget, instance_mask, order_out)
@@ -320,18 +414,15 @@ def _check_opts(opts: rb_options, B: int, I: int):
 
 def rb_assign_ex(q_hat, l_hat, prompt_len, inst: DeviceInstances, weights, opts: rb_options,
                  assign: Optional[torch.Tensor] = None, chosen: Optional[torch.Tensor] = None,
-                 stream=None, want_chosen: bool = True):
-    B, M = q_hat.shape
-    dev = q_hat.device
-    if assign is None:
-        assign = torch.empty(B, dtype=torch.int32, device=dev)
-    if chosen is None and want_chosen:
-        chosen = torch.empty(B, dtype=torch.float32, device=dev)
+                 stream=None, want_chosen: bool = True, decided: Optional[torch.Tensor] = None):
+    B, M = _request_args(q_hat, l_hat, prompt_len)
+    assign, chosen = _assign_outputs(B, inst.I, q_hat.device, assign, chosen, decided,
+                                     want_chosen)
     _check_opts(opts, B, inst.I)
     s = inst.struct()
     _check(_lib.rb_assign_ex(_ptr(q_hat), _ptr(l_hat), _ptr(prompt_len), B, M, ctypes.byref(s),
                              inst.I, _w(weights), ctypes.byref(opts), _ptr(assign), _ptr(chosen),
-                             _stream(stream)), "rb_assign_ex")
+                             _ptr(decided), _stream(stream)), "rb_assign_ex")
     return assign, chosen
 
 
@@ -346,9 +437,14 @@ def rb_knn_predict(queries, bank, bank_norms, k: int, bank_qual, bank_len,
     run (their lists stay in ``ws``; returns (None, None) unless buffers are
     given); with RB_FLAG_FROM_LISTS only the merge and average of the lists a
     LISTS_ONLY call left in ``ws`` (the same shapes and overlap flag)."""
-    B, d = queries.shape
-    N = bank.shape[0]
-    M = bank_qual.shape[1]
+    B, N, d = _embeddings(queries, bank)
+    _expect(bank_norms, torch.float32, (N,), "bank_norms")
+    M = _labels(bank_qual, bank_len, N)
+    _expect_opt(q_hat, torch.float32, (B, M), "q_hat")
+    _expect_opt(l_hat, torch.float32, (B, M), "l_hat")
+    _expect_opt(nbr_idx, torch.int32, (B, k), "nbr_idx")
+    _expect_opt(nbr_dist, torch.float32, (B, k), "nbr_dist")
+    _expect_opt(ws, torch.uint8, (ws.numel(),) if ws is not None else (), "ws")
     dev = queries.device
     lists_only = opts is not None and (opts.flags & RB_FLAG_LISTS_ONLY)
     if q_hat is None and not lists_only:
@@ -372,11 +468,10 @@ def rb_route_batch_ex(queries, bank, bank_norms, k: int, bank_qual, bank_len, pr
                       nbr_idx: Optional[torch.Tensor] = None,
                       nbr_dist: Optional[torch.Tensor] = None,
                       q_hat: Optional[torch.Tensor] = None, l_hat: Optional[torch.Tensor] = None,
-                      stream=None):
+                      stream=None, score0: Optional[torch.Tensor] = None):
     """rb_route_batch with options (order, weighting, budgets, availability)."""
-    B, d = queries.shape
-    N = bank.shape[0]
-    M = bank_qual.shape[1]
+    B, N, d, M = _route_args(queries, bank, bank_norms, k, bank_qual, bank_len, prompt_len, inst,
+                             ws, nbr_idx, nbr_dist, q_hat, l_hat, score0, chosen, assign)
     dev = queries.device
     if assign is None:
         assign = torch.empty(B, dtype=torch.int32, device=dev)
@@ -388,8 +483,8 @@ def rb_route_batch_ex(queries, bank, bank_norms, k: int, bank_qual, bank_len, pr
                                   B, N, d, k, _ptr(bank_qual), _ptr(bank_len), M,
                                   _ptr(prompt_len), ctypes.byref(s), inst.I, _w(weights),
                                   ctypes.byref(opts), _ptr(assign), _ptr(chosen), _ptr(nbr_idx),
-                                  _ptr(nbr_dist), _ptr(q_hat), _ptr(l_hat), _ptr(ws), ws.numel(),
-                                  _stream(stream)), "rb_route_batch_ex")
+                                  _ptr(nbr_dist), _ptr(q_hat), _ptr(l_hat), _ptr(score0),
+                                  _ptr(ws), ws.numel(), _stream(stream)), "rb_route_batch_ex")
     return assign
 
 

@@ -140,7 +140,8 @@ rb_status check_opts(const rb_options *o, uint32_t flags_ok = RB_FLAG_OVERLAP)
 // loop over it.
 hipError_t enqueue_assign(const float *qh, const float *lh, const int32_t *plen, int B, int M,
                           const rb_instances *inst, int I, rb_weights w, const rb_options *o,
-                          int32_t *order, int32_t *assign, float *chosen, hipStream_t st)
+                          int32_t *order, int32_t *assign, float *chosen, float *decided,
+                          hipStream_t st)
 {
     rb::AssignOpts ao;
     ao.order = nullptr;
@@ -153,7 +154,21 @@ hipError_t enqueue_assign(const float *qh, const float *lh, const int32_t *plen,
         ao.order = order;
     }
     return rb::launch_assign(qh, lh, plen, B, M, inst_args(inst), I, w.w_qual, w.w_lat, w.w_cost,
-                             ao, assign, chosen, st);
+                             ao, assign, chosen, decided, st);
+}
+
+// The dense score matrix at the current state over each request's candidate
+// set (the options' budgets and mask).
+hipError_t enqueue_score(const float *qh, const float *lh, const int32_t *plen, int B, int M,
+                         const rb_instances *inst, int I, rb_weights w, const rb_options *o,
+                         float *score0, hipStream_t st)
+{
+    rb::AssignOpts ao;
+    ao.order = nullptr;
+    ao.budget = o->budget;
+    ao.mask = o->instance_mask;
+    return rb::launch_score(qh, lh, plen, B, M, inst_args(inst), I, w.w_qual, w.w_lat, w.w_cost,
+                            ao, score0, st);
 }
 
 // The KNN plan on the current device. With `overlap`, the scan leaves one
@@ -178,7 +193,8 @@ rb_status route_batch(const void *queries, const void *bank, const float *bank_n
                       const float *bank_len, int M, const int32_t *prompt_len,
                       const rb_instances *inst, int I, rb_weights w, const rb_options *o,
                       int32_t *assign, float *chosen_score, int32_t *nbr_idx, float *nbr_dist,
-                      float *q_hat, float *l_hat, void *ws, size_t ws_bytes, void *stream)
+                      float *q_hat, float *l_hat, float *score0, void *ws, size_t ws_bytes,
+                      void *stream)
 {
     rb_status s = check_knn_dims(dtype, B, N, d, k);
     if (s != RB_OK)
@@ -215,7 +231,11 @@ rb_status route_batch(const void *queries, const void *bank, const float *bank_n
                                   bank_len, M, qh, lh, o->weighting == RB_KNN_INV_DIST, st);
     if (e != hipSuccess)
         return RB_ERR_HIP;
-    e = enqueue_assign(qh, lh, prompt_len, B, M, inst, I, w, o, order, assign, chosen_score, st);
+    if (score0 &&
+        (e = enqueue_score(qh, lh, prompt_len, B, M, inst, I, w, o, score0, st)) != hipSuccess)
+        return RB_ERR_HIP;
+    e = enqueue_assign(qh, lh, prompt_len, B, M, inst, I, w, o, order, assign, chosen_score,
+                       nullptr, st);
     if (e == hipSuccess && o->order != RB_ORDER_LPT && o->order_out)
         e = rb::launch_iota(o->order_out, B, st);
     return hip_status(e);
@@ -328,14 +348,13 @@ rb_status rb_score(const float *q_hat, const float *l_hat, const int32_t *prompt
         return RB_OK;
     if (!q_hat || !l_hat || !prompt_len || !score0)
         return RB_ERR_NULL;
-    return hip_status(rb::launch_score(q_hat, l_hat, prompt_len, B, M, inst_args(inst), I,
-                                       w.w_qual, w.w_lat, w.w_cost, score0,
-                                       (hipStream_t)stream));
+    return hip_status(enqueue_score(q_hat, l_hat, prompt_len, B, M, inst, I, w, &k_default_opts,
+                                    score0, (hipStream_t)stream));
 }
 
 rb_status rb_assign(const float *q_hat, const float *l_hat, const int32_t *prompt_len, int B,
                     int M, const rb_instances *inst, int I, rb_weights w, int32_t *assign,
-                    float *chosen_score, void *stream)
+                    float *chosen_score, float *decided, void *stream)
 {
     if (B < 0 || M < 1 || M > RB_MAX_M)
         return RB_ERR_DIMS;
@@ -349,13 +368,14 @@ rb_status rb_assign(const float *q_hat, const float *l_hat, const int32_t *promp
     if (!q_hat || !l_hat || !prompt_len || !assign)
         return RB_ERR_NULL;
     return hip_status(enqueue_assign(q_hat, l_hat, prompt_len, B, M, inst, I, w, &k_default_opts,
-                                     nullptr, assign, chosen_score, (hipStream_t)stream));
+                                     nullptr, assign, chosen_score, decided,
+                                     (hipStream_t)stream));
 }
 
 rb_status rb_assign_ex(const float *q_hat, const float *l_hat, const int32_t *prompt_len, int B,
                        int M, const rb_instances *inst, int I, rb_weights w,
                        const rb_options *opts, int32_t *assign, float *chosen_score,
-                       void *stream)
+                       float *decided, void *stream)
 {
     const rb_options *o = opts ? opts : &k_default_opts;
     if (B < 0 || M < 1 || M > RB_MAX_M)
@@ -375,7 +395,7 @@ rb_status rb_assign_ex(const float *q_hat, const float *l_hat, const int32_t *pr
         return RB_ERR_NULL;
     hipStream_t st = (hipStream_t)stream;
     hipError_t e = enqueue_assign(q_hat, l_hat, prompt_len, B, M, inst, I, w, o, o->order_out,
-                                  assign, chosen_score, st);
+                                  assign, chosen_score, decided, st);
     if (e == hipSuccess && o->order != RB_ORDER_LPT && o->order_out)
         e = rb::launch_iota(o->order_out, B, st);
     return hip_status(e);
@@ -427,11 +447,11 @@ rb_status rb_route_batch(const void *queries, const void *bank, const float *ban
                          const float *bank_len, int M, const int32_t *prompt_len,
                          const rb_instances *inst, int I, rb_weights w, int32_t *assign,
                          float *chosen_score, int32_t *nbr_idx, float *nbr_dist, float *q_hat,
-                         float *l_hat, void *ws, size_t ws_bytes, void *stream)
+                         float *l_hat, float *score0, void *ws, size_t ws_bytes, void *stream)
 {
     return route_batch(queries, bank, bank_norms, dtype, B, N, d, k, bank_qual, bank_len, M,
                        prompt_len, inst, I, w, &k_default_opts, assign, chosen_score, nbr_idx,
-                       nbr_dist, q_hat, l_hat, ws, ws_bytes, stream);
+                       nbr_dist, q_hat, l_hat, score0, ws, ws_bytes, stream);
 }
 
 rb_status rb_route_batch_ex(const void *queries, const void *bank, const float *bank_norms,
@@ -440,11 +460,12 @@ rb_status rb_route_batch_ex(const void *queries, const void *bank, const float *
                             const rb_instances *inst, int I, rb_weights w,
                             const rb_options *opts, int32_t *assign, float *chosen_score,
                             int32_t *nbr_idx, float *nbr_dist, float *q_hat, float *l_hat,
-                            void *ws, size_t ws_bytes, void *stream)
+                            float *score0, void *ws, size_t ws_bytes, void *stream)
 {
     return route_batch(queries, bank, bank_norms, dtype, B, N, d, k, bank_qual, bank_len, M,
                        prompt_len, inst, I, w, opts ? opts : &k_default_opts, assign,
-                       chosen_score, nbr_idx, nbr_dist, q_hat, l_hat, ws, ws_bytes, stream);
+                       chosen_score, nbr_idx, nbr_dist, q_hat, l_hat, score0, ws, ws_bytes,
+                       stream);
 }
 
 rb_status rb_profile_scan_events(void *begin, void *end)

@@ -102,9 +102,6 @@ struct InstArgs {
     const float *P, *D, *cin, *cout;
 };
 
-hipError_t launch_score(const float *q_hat, const float *l_hat, const int32_t *plen, int B, int M,
-                        const InstArgs &in, int I, float wq, float wl, float wc, float *S0,
-                        hipStream_t s);
 // Options of the greedy loop; null pointers are the defaults (arrival order,
 // no budgets, every instance available).
 struct AssignOpts {
@@ -113,12 +110,19 @@ struct AssignOpts {
     const uint8_t *mask;     // [I] nonzero = available
 };
 
+// The dense score matrix; opt's budget and mask restrict each row's
+// candidates (its order is not read).
+hipError_t launch_score(const float *q_hat, const float *l_hat, const int32_t *plen, int B, int M,
+                        const InstArgs &in, int I, float wq, float wl, float wc,
+                        const AssignOpts &opt, float *S0, hipStream_t s);
+
 hipError_t launch_lpt_order(const float *l_hat, int B, int M, int32_t *order, hipStream_t s);
 // out[i] = i for i < n (the arrival order, when the caller asks for it).
 hipError_t launch_iota(int32_t *out, int n, hipStream_t s);
 hipError_t launch_assign(const float *q_hat, const float *l_hat, const int32_t *plen, int B,
                          int M, const InstArgs &in, int I, float wq, float wl, float wc,
-                         const AssignOpts &opt, int32_t *assign, float *chosen, hipStream_t s);
+                         const AssignOpts &opt, int32_t *assign, float *chosen, float *decided,
+                         hipStream_t s);
 hipError_t launch_advance(const InstArgs &in, int I, float dt, hipStream_t s);
 
 }  // namespace rb

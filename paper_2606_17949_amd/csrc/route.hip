@@ -45,12 +45,23 @@ __device__ __forceinline__ float full_score(float base, float T, float tmax, flo
     return fmaf(wl, 1.f - ratio(T, tmax), base);
 }
 
-// One wave per request row of the dense score matrix.
+// Alg. 1 budget filter on the Eq. 2 cost C of a request with budget b, and
+// the availability mask: whether instance i is a candidate.
+__device__ __forceinline__ bool admitted(float C, float b, const uint8_t *mask, int i)
+{
+    return (!mask || mask[i] != 0) && C <= b;
+}
+
+// One wave per request row of the dense score matrix. With a budget or a
+// mask (opt.budget, opt.mask; opt.order is not read) the maxima run over the
+// request's candidates and the other instances score NaN, as in the greedy
+// loop's first step.
 __global__ __launch_bounds__(256) void score_kernel(const float *__restrict__ q_hat,
                                                     const float *__restrict__ l_hat,
                                                     const int32_t *__restrict__ plen, int B, int M,
                                                     const InstArgs in, int I, float wq, float wl,
-                                                    float wc, float *__restrict__ S0)
+                                                    float wc, const AssignOpts opt,
+                                                    float *__restrict__ S0)
 {
     const int lane = lane_id();
     const int r = (blockIdx.x * blockDim.x + threadIdx.x) >> 6;
@@ -60,11 +71,15 @@ __global__ __launch_bounds__(256) void score_kernel(const float *__restrict__ q_
     const float *qr = q_hat + (size_t)r * M;
     const float *lr = l_hat + (size_t)r * M;
     const float nan = __builtin_nanf("");
+    const float budget = opt.budget ? opt.budget[r] : INFINITY;
     float cmax = -INFINITY, tmax = -INFINITY;
     for (int i = lane; i < I; i += WAVE) {
         const int m = in.model[i];
         const float lv = (unsigned)m < (unsigned)M ? lr[m] : nan;
-        cmax = fmaxf(cmax, cost(l, lv, in.cin[i], in.cout[i]));
+        const float C = cost(l, lv, in.cin[i], in.cout[i]);
+        if (!admitted(C, budget, opt.mask, i))
+            continue;
+        cmax = fmaxf(cmax, C);
         tmax = fmaxf(tmax, latency(in.p[i], in.a[i], 1.f / in.P[i], 1.f / in.D[i], l, lv));
     }
     cmax = wave_max(cmax);
@@ -76,7 +91,9 @@ __global__ __launch_bounds__(256) void score_kernel(const float *__restrict__ q_
         const float qv = mv ? qr[m] : nan;
         const float C = cost(l, lv, in.cin[i], in.cout[i]);
         const float T = latency(in.p[i], in.a[i], 1.f / in.P[i], 1.f / in.D[i], l, lv);
-        S0[(size_t)r * I + i] = full_score(base_score(qv, C, cmax, wq, wc), T, tmax, wl);
+        S0[(size_t)r * I + i] = admitted(C, budget, opt.mask, i)
+                                    ? full_score(base_score(qv, C, cmax, wq, wc), T, tmax, wl)
+                                    : nan;
     }
 }
 
@@ -152,7 +169,8 @@ template <int IPL, int WIDTH>
 __global__ __launch_bounds__(assign_threads<IPL>()) void assign_kernel(
     const float *__restrict__ q_hat, const float *__restrict__ l_hat,
     const int32_t *__restrict__ plen, int B, int M, const InstArgs in, int I, float wq, float wl,
-    float wc, const AssignOpts opt, int32_t *__restrict__ assign, float *__restrict__ chosen)
+    float wc, const AssignOpts opt, int32_t *__restrict__ assign, float *__restrict__ chosen,
+    float *__restrict__ decided)
 {
     static_assert(WIDTH == 64 || IPL == 1, "a 16-lane row holds one slot");
     constexpr int IP = IPL * WIDTH;                       // instances per LDS row
@@ -198,7 +216,7 @@ __global__ __launch_bounds__(assign_threads<IPL>()) void assign_kernel(
                 lv[u] = ok ? lr[m] : 0.f;
                 C[u] = cost(l, lv[u], ok ? in.cin[i] : 0.f, ok ? in.cout[i] : 0.f);
                 // Alg. 1 budget filter on the Eq. 2 cost, and availability
-                cand[u] = ok && (!opt.mask || opt.mask[i] != 0) && C[u] <= budget;
+                cand[u] = ok && admitted(C[u], budget, opt.mask, i);
                 if (cand[u])
                     cmax = fmaxf(cmax, C[u]);
             }
@@ -339,6 +357,20 @@ __global__ __launch_bounds__(assign_threads<IPL>()) void assign_kernel(
                     cap_b = mine ? vb : cap_b;
                     cap_t = mine ? vt : cap_t;
                 }
+                if (decided) {
+                    // the row of Eq. 1 scores this step saw, at the state
+                    // before its update (NaN outside the candidate set), with
+                    // the division of the dense score kernel
+                    const int rq = __builtin_amdgcn_readlane(rblk, slot);
+                    float *drow = decided + (size_t)rq * I;
+#pragma unroll
+                    for (int u = 0; u < IPL; ++u) {
+                        const int i = inst(u);
+                        if (lane < (WIDTH == 16 ? 16 : WAVE) && i < I)
+                            drow[i] = bs[u] == bs[u] ? full_score(bs[u], T[u], tmax, wl)
+                                                     : __builtin_nanf("");
+                    }
+                }
 #pragma unroll
                 for (int u = 0; u < IPL; ++u) {
                     if (inst(u) == istar) {
@@ -391,11 +423,11 @@ __global__ __launch_bounds__(256) void advance_kernel(const InstArgs in, int I, 
 }  // namespace
 
 hipError_t launch_score(const float *q_hat, const float *l_hat, const int32_t *plen, int B, int M,
-                        const InstArgs &in, int I, float wq, float wl, float wc, float *S0,
-                        hipStream_t s)
+                        const InstArgs &in, int I, float wq, float wl, float wc,
+                        const AssignOpts &opt, float *S0, hipStream_t s)
 {
     hipLaunchKernelGGL(score_kernel, dim3((B + 3) / 4), dim3(256), 0, s, q_hat, l_hat, plen, B, M,
-                       in, I, wq, wl, wc, S0);
+                       in, I, wq, wl, wc, opt, S0);
     return hipGetLastError();
 }
 
@@ -408,12 +440,13 @@ hipError_t launch_lpt_order(const float *l_hat, int B, int M, int32_t *order, hi
 
 hipError_t launch_assign(const float *q_hat, const float *l_hat, const int32_t *plen, int B,
                          int M, const InstArgs &in, int I, float wq, float wl, float wc,
-                         const AssignOpts &opt, int32_t *assign, float *chosen, hipStream_t s)
+                         const AssignOpts &opt, int32_t *assign, float *chosen, float *decided,
+                         hipStream_t s)
 {
     const int ipl = (I + WAVE - 1) / WAVE;
 #define RB_ASSIGN(N, W)                                                                          \
     hipLaunchKernelGGL((assign_kernel<N, W>), dim3(1), dim3(assign_threads<N>()), 0, s, q_hat,   \
-                       l_hat, plen, B, M, in, I, wq, wl, wc, opt, assign, chosen)
+                       l_hat, plen, B, M, in, I, wq, wl, wc, opt, assign, chosen, decided)
     if (I <= 16) RB_ASSIGN(1, 16);
     else if (ipl <= 1) RB_ASSIGN(1, 64);
     else if (ipl <= 2) RB_ASSIGN(2, 64);

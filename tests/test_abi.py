@@ -119,7 +119,8 @@ def test_score_and_assign_reject_off_simplex_weights(w):
     s = _inst()
     ww = rb.rb_weights(*w)
     assert L.rb_score(FAKE, FAKE, FAKE, 4, 4, ctypes.byref(s), 13, ww, FAKE, None) == rb.RB_ERR_WEIGHTS
-    assert L.rb_assign(FAKE, FAKE, FAKE, 4, 4, ctypes.byref(s), 13, ww, FAKE, None, None) == \
+    assert L.rb_assign(FAKE, FAKE, FAKE, 4, 4, ctypes.byref(s), 13, ww, FAKE, None, None,
+                       None) == \
         rb.RB_ERR_WEIGHTS
 
 
@@ -136,14 +137,16 @@ def test_score_assign_instance_validation():
     assert L.rb_score(FAKE, FAKE, FAKE, 4, 4, None, 13, W, FAKE, None) == rb.RB_ERR_NULL
     for f in rb.DeviceInstances.FIELDS:
         s = _inst(**{f: None})
-        assert L.rb_assign(FAKE, FAKE, FAKE, 4, 4, ctypes.byref(s), 13, W, FAKE, None, None) == \
+        assert L.rb_assign(FAKE, FAKE, FAKE, 4, 4, ctypes.byref(s), 13, W, FAKE, None, None,
+                           None) == \
             rb.RB_ERR_NULL, f
     s = _inst()
     assert L.rb_score(FAKE, FAKE, FAKE, 4, 4, ctypes.byref(s), 0, W, FAKE, None) == rb.RB_ERR_DIMS
     assert L.rb_score(FAKE, FAKE, FAKE, 4, 4, ctypes.byref(s), 1025, W, FAKE, None) == \
         rb.RB_ERR_DIMS
     assert L.rb_score(FAKE, FAKE, FAKE, 4, 0, ctypes.byref(s), 13, W, FAKE, None) == rb.RB_ERR_DIMS
-    assert L.rb_assign(FAKE, FAKE, FAKE, 4, 4, ctypes.byref(s), 13, W, None, None, None) == \
+    assert L.rb_assign(FAKE, FAKE, FAKE, 4, 4, ctypes.byref(s), 13, W, None, None, None,
+                       None) == \
         rb.RB_ERR_NULL
 
 
@@ -156,7 +159,7 @@ def test_route_batch_validation():
         a.update(kw)
         return L.rb_route_batch(a["q"], a["x"], a["n"], a["dt"], a["B"], a["N"], a["d"], a["k"],
                                 a["qual"], a["ln"], a["M"], a["pl"], a["inst"], a["I"], a["w"],
-                                a["asg"], None, None, None, None, None, FAKE, 1 << 20, None)
+                                a["asg"], None, None, None, None, None, None, FAKE, 1 << 20, None)
     assert call(k=11, N=10) == rb.RB_ERR_DIMS
     assert call(M=0) == rb.RB_ERR_DIMS
     assert call(I=0) == rb.RB_ERR_DIMS
@@ -176,7 +179,7 @@ def test_assign_ex_validation():
         a.update(kw)
         o = None if opts is None else ctypes.byref(opts)
         return L.rb_assign_ex(a["q"], FAKE, FAKE, a["B"], a["M"], a["inst"], a["I"], a["w"], o,
-                              a["asg"], None, None)
+                              a["asg"], None, None, None)
     assert call(rb.rb_options(2, 0, None, None, None)) == rb.RB_ERR_UNSUPPORTED
     assert call(rb.rb_options(0, 5, None, None, None)) == rb.RB_ERR_UNSUPPORTED
     assert call(rb.rb_options(-1, 0, None, None, None)) == rb.RB_ERR_UNSUPPORTED
@@ -201,7 +204,7 @@ def test_route_batch_ex_validation():
         return L.rb_route_batch_ex(a["q"], FAKE, FAKE, rb.RB_BF16, a["B"], 100, 64, 10, FAKE, FAKE,
                                    4, FAKE, ctypes.byref(s), 13, W,
                                    None if opts is None else ctypes.byref(opts), a["asg"], None,
-                                   None, None, None, None, FAKE, 1 << 20, None)
+                                   None, None, None, None, None, FAKE, 1 << 20, None)
     assert call(rb.rb_options(3, 0, None, None, None)) == rb.RB_ERR_UNSUPPORTED
     assert call(rb.rb_options(0, 3, None, None, None)) == rb.RB_ERR_UNSUPPORTED
     # the split-lookup flags belong to rb_knn_predict only

@@ -5,6 +5,8 @@ oracle.parity: neighbours exact up to boundary near-ties within 1e-5, values
 within 1e-4, assignments teacher-forced with near-ties within 1e-5 and
 bit-identical free-running picks when no near tie occurred.
 """
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -119,6 +121,40 @@ def test_knn_exact_ties_take_lower_index():
     assert np.all(gd == 64.0)
 
 
+@pytest.mark.parametrize("label,B,N,d,k", [
+    ("query-resident scan", 200, 70000, 768, 10),
+    ("seeded tile scan, one tile", 64, 70000, 768, 10),
+    ("seeded tile scan, two tiles", 300, 66000, 256, 16),
+])
+def test_knn_exact_ties_across_kth(label, B, N, d, k):
+    """Duplicated rows straddling the k-th position: each request's k-th
+    neighbour is copied into two other rows, one lower and one higher where
+    the bank allows, spread over the bank's chunks. The three rows are at
+    exactly the same distance on both sides, so only the lowest index may be
+    in the list; the extended oracle lists make check_neighbours enforce it."""
+    say(f"knn exact ties across k: {label} B={B} N={N} d={d} k={k}")
+    q, x = clustered(B, N, d, "bf16", seed=N + B, plant=False)
+    oi, _ = oracle.knn(q, x, k + 2, nthreads=16)
+    rng = np.random.default_rng(B)
+    used = set(oi.ravel().tolist())
+    free = np.array([n for n in rng.permutation(N) if n not in used])
+    fi = 0
+    for b in range(B):
+        src = int(oi[b, k - 1])
+        lo = free[fi:][free[fi:] < src][:1]
+        hi = free[fi:][free[fi:] > src][:1]
+        for j in np.concatenate([lo, hi]):
+            x[int(j)] = x[src]
+            free = free[free != j]
+    oi, od = oracle.knn(q, x, k + 4, nthreads=16)
+    straddle = int(np.sum(od[:, k - 1] == od[:, k]))
+    say(f"  requests with an exact tie across the k-th position: {straddle}/{B}")
+    assert straddle >= B // 2
+    gi, gd = gpu_knn(q, x, k)
+    ties = par.check_neighbours(gi, gd, oi, od, label=label)
+    say(f"  boundary near-ties: {ties}")
+
+
 def test_knn_deterministic():
     say("knn determinism")
     q, x = clustered(70, 20000, 256, "bf16", seed=9)
@@ -204,15 +240,48 @@ def test_assign_parity(B, M, I, w):
     say(f"assign B={B} M={M} I={I} w={w}")
     qh, lh, pl, inst = random_route_case(B, M, I, seed=B * 7 + I)
     gi = rb().DeviceInstances.from_host(inst, DEV)
-    asg, ch = rb().rb_assign(dev(qh), dev(lh), dev(pl), gi, w)
+    decided = torch.empty(B, I, device=DEV)
+    asg, ch = rb().rb_assign(dev(qh), dev(lh), dev(pl), gi, w, decided=decided)
     torch.cuda.synchronize()
-    near = par.check_assign(asg.cpu().numpy(), ch.cpu().numpy(), qh, lh, pl, inst, w,
+    a_h, c_h, d_h = asg.cpu().numpy(), ch.cpu().numpy(), decided.cpu().numpy()
+    near = par.check_assign(a_h, c_h, qh, lh, pl, inst, w,
                             g_final_p=gi.prefill_q.cpu().numpy(),
-                            g_final_a=gi.decode_q.cpu().numpy())
+                            g_final_a=gi.decode_q.cpu().numpy(), g_decided=d_h)
+    # the chosen score is the decided row's entry at the pick, bit for bit
+    assert np.array_equal(c_h.view(np.uint32), d_h[np.arange(B), a_h].view(np.uint32))
+    # the first row was decided at the batch-start state: rb_score's row
+    S0 = rb().rb_score(dev(qh), dev(lh), dev(pl), rb().DeviceInstances.from_host(inst, DEV), w)
+    torch.cuda.synchronize()
+    assert np.array_equal(S0.cpu().numpy()[0].view(np.uint32), d_h[0].view(np.uint32))
     free = oracle.assign(qh.astype(np.float64), lh.astype(np.float64), pl, inst, w)
     if near == 0:
-        assert np.array_equal(free["assign"], asg.cpu().numpy())
+        assert np.array_equal(free["assign"], a_h)
     say(f"  near-ties {near}")
+
+
+def test_zero_prices_on_gpu():
+    # every price zero: the cost maximum is zero, so the cost ratio is 0 and
+    # the cost term adds w_cost to every instance (the zero-maximum reading);
+    # with w = (0, 0, 1) every score is 1 and the lowest index wins
+    say("zero prices")
+    qh, lh, pl, inst = random_route_case(40, 4, 13, seed=77)
+    inst.price_in[:] = 0
+    inst.price_out[:] = 0
+    for w in [(0, 0, 1), (0.4, 0.3, 0.3), (0.1, 0.2, 0.7)]:
+        gi = rb().DeviceInstances.from_host(inst, DEV)
+        S0 = rb().rb_score(dev(qh), dev(lh), dev(pl), gi, w)
+        decided = torch.empty(40, 13, device=DEV)
+        asg, ch = rb().rb_assign(dev(qh), dev(lh), dev(pl), gi, w, decided=decided)
+        torch.cuda.synchronize()
+        par.check_scores(S0.cpu().numpy(), qh, lh, pl, inst, w)
+        near = par.check_assign(asg.cpu().numpy(), ch.cpu().numpy(), qh, lh, pl, inst, w,
+                                g_final_p=gi.prefill_q.cpu().numpy(),
+                                g_final_a=gi.decode_q.cpu().numpy(),
+                                g_decided=decided.cpu().numpy())
+        if w == (0, 0, 1):
+            assert np.all(S0.cpu().numpy() == 1.0)
+            assert np.all(asg.cpu().numpy() == 0)
+        say(f"  w={w} near-ties {near}")
 
 
 def test_assign_hand_example_on_gpu():
@@ -275,10 +344,11 @@ def run_route(cfg, bank, queries, qual, ln, pl, inst, norms=None):
     gi = m.DeviceInstances.from_host(inst, DEV)
     out = dict(nbr=torch.empty(B, k, dtype=torch.int32, device=DEV),
                nd=torch.empty(B, k, device=DEV), qh=torch.empty(B, M, device=DEV),
-               lh=torch.empty(B, M, device=DEV), ch=torch.empty(B, device=DEV))
+               lh=torch.empty(B, M, device=DEV), ch=torch.empty(B, device=DEV),
+               s0=torch.empty(B, gi.I, device=DEV))
     asg = m.rb_route_batch(queries.to(DEV), gb, norms, k, dev(qual), dev(ln), dev(pl), gi,
                            cfg.weights, chosen=out["ch"], nbr_idx=out["nbr"], nbr_dist=out["nd"],
-                           q_hat=out["qh"], l_hat=out["lh"])
+                           q_hat=out["qh"], l_hat=out["lh"], score0=out["s0"])
     torch.cuda.synchronize()
     res = {kk: v.cpu().numpy() for kk, v in out.items()}
     res["assign"] = asg.cpu().numpy()
@@ -288,12 +358,15 @@ def run_route(cfg, bank, queries, qual, ln, pl, inst, norms=None):
 
 
 def check_route(cfg, res, queries, bank, qual, ln, pl, inst, rows=None, label=""):
+    # the oracle lists run 4 past k: they decide exact ties across the k-th
+    threads = len(os.sched_getaffinity(0))
     if rows is None:
-        oi, od = oracle.knn(queries, bank, cfg.k, nthreads=16)
+        oi, od = oracle.knn(queries, bank, cfg.k + 4, nthreads=threads)
     else:
-        oi, od = oracle.knn(queries[rows], bank, cfg.k, nthreads=16)
+        oi, od = oracle.knn(queries[rows], bank, cfg.k + 4, nthreads=threads)
     ties = par.check_neighbours(res["nbr"], res["nd"], oi, od, rows=rows, label=label)
     par.check_predictions(res["nbr"], res["qh"], res["lh"], qual, ln, label=label)
+    par.check_scores(res["s0"], res["qh"], res["lh"], pl, inst, cfg.weights, label=label)
     near = par.check_assign(res["assign"], res["ch"], res["qh"], res["lh"], pl, inst, cfg.weights,
                             g_final_p=res["p"], g_final_a=res["a"], label=label)
     return ties, near
@@ -329,13 +402,15 @@ def test_route_batch_end_to_end(name, over):
 # ----------------------------------------------------------------------------- full sizes
 
 
-@pytest.mark.parametrize("name,sample", [("online", None), ("highload", 8), ("largebatch", 4),
-                                         ("wide", 4), ("stream64", 8)])
-def test_full_size_sampled_parity(name, sample):
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("name,sample", [("online", None), ("highload", None),
+                                         ("largebatch", None), ("wide", None),
+                                         ("stream64", None)])
+def test_full_size_parity(name, sample):
     """The workloads at their real sizes, in the configuration the benchmark
-    times. The oracle recomputes every prediction, score and pick (teacher
-    forced) and the neighbour lists of all requests (online) or of a spread
-    sample of them."""
+    times. The oracle recomputes every request's neighbour list (exact, on
+    all host threads: up to about a minute for the largebatch workload), and
+    every prediction, score and pick (teacher forced)."""
     cfg = synth.CONFIGS[name]
     say(f"full-size {name}: B={cfg.B} N={cfg.N} d={cfg.d} M={cfg.M} I={cfg.I}")
     centres = synth.make_centres(cfg, DEV)

@@ -76,10 +76,13 @@ def run_assign_ex(qh, lh, pl, inst, w, order=0, budget=None, mask=None):
 
 
 def check(res, qh, lh, pl, inst, w, order, budget=None, mask=None, label=""):
+    st = {}
     near = par.check_assign(res["assign"], res["chosen"], qh, lh, pl, inst, w,
                             g_final_p=res["p"], g_final_a=res["a"], label=label,
                             order="lpt" if order == rb().RB_ORDER_LPT else "arrival",
-                            g_order=res["order"], budget=budget, mask=mask)
+                            g_order=res["order"], budget=budget, mask=mask, stats=st)
+    if budget is not None:
+        say(f"  {label}: near-ties {st}")
     free = oracle.assign(qh.astype(np.float64), lh.astype(np.float64), pl, inst, w,
                          order="lpt" if order == rb().RB_ORDER_LPT else "arrival",
                          budget=budget, mask=mask)
@@ -181,6 +184,41 @@ def test_budget_boundary_is_inclusive_on_gpu():
     check(res, qh, lh, pl, inst, (0.3, 0.4, 0.3), 0, budget=budget, label="boundary")
     assert np.all(res["assign"] >= 0)            # the budget's own instance is admitted
     assert np.all(C[np.arange(B), res["assign"]] <= budget)
+
+
+def _fmaf():
+    import ctypes
+    import ctypes.util
+    libm = ctypes.CDLL(ctypes.util.find_library("m"))
+    libm.fmaf.restype = ctypes.c_float
+    libm.fmaf.argtypes = [ctypes.c_float] * 3
+    return libm.fmaf
+
+
+@pytest.mark.parametrize("nudge", [-1, 0, 1])
+def test_budget_at_the_fp32_cost_boundary(nudge):
+    """Budgets placed on an instance's cost as fp32 evaluates it (one fused
+    multiply-add), nudged by nudge ulps: the exact Eq. 2 cost that the oracle
+    compares lies within rounding of the budget, so either admission is
+    acceptable there (a counted boundary near-tie); every other instance's
+    admission must match the oracle's exactly."""
+    say(f"budget on the fp32 cost boundary, nudge {nudge} ulp")
+    B, M, I = 200, 4, 13
+    qh, lh, pl, inst = random_case(B, M, I, seed=31 + nudge)
+    fmaf = _fmaf()
+    rng = np.random.default_rng(8)
+    pick = rng.integers(0, I, B)
+    budget = np.empty(B, np.float32)
+    for r in range(B):
+        i = pick[r]
+        prod = np.float32(np.float32(lh[r, inst.model[i]]) * np.float32(inst.price_out[i]))
+        c32 = np.float32(fmaf(float(pl[r]), float(inst.price_in[i]), float(prod)))
+        for _ in range(abs(nudge)):
+            c32 = np.nextafter(c32, np.float32(np.inf if nudge > 0 else -np.inf))
+        budget[r] = c32
+    for w in [(0.3, 0.4, 0.3), (0, 0, 1)]:
+        res = run_assign_ex(qh, lh, pl, inst, w, budget=budget)
+        check(res, qh, lh, pl, inst, w, 0, budget=budget, label=f"w={w} nudge={nudge}")
 
 
 def test_budget_mask_hand_example_on_gpu():
