@@ -51,7 +51,9 @@ typedef enum {
     RB_ERR_WORKSPACE = -5,   /* workspace NULL or smaller than rb_workspace_size */
     RB_ERR_UNSUPPORTED = -6, /* an option this version does not implement */
     RB_ERR_HIP = -7,         /* a HIP runtime call or kernel launch failed */
-    RB_ERR_ALIGN = -8        /* a pointer is not aligned as required */
+    RB_ERR_ALIGN = -8,       /* a pointer is not aligned as required */
+    RB_ERR_SCRATCH = -9      /* rb_route_batch_noalloc: these sizes need more workspace than
+                                RB_SCRATCH_BYTES */
 } rb_status;
 
 typedef enum { RB_F32 = 0, RB_BF16 = 1 } rb_dtype;
@@ -314,6 +316,34 @@ rb_status rb_route_batch_ex(const void *queries, const void *bank, const float *
                             const rb_options *opts, int32_t *assign, float *chosen_score,
                             int32_t *nbr_idx, float *nbr_dist, float *q_hat, float *l_hat,
                             float *score0, void *ws, size_t ws_bytes, void *stream);
+
+/* Bytes of the library's own per-GPU workspace used by rb_route_batch_noalloc. */
+#define RB_SCRATCH_BYTES (64u << 20)
+
+/* rb_route_batch for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation.
+ * The arguments and results are those of rb_route_batch without ws and
+ * ws_bytes; the workspace is instead a static device array of
+ * RB_SCRATCH_BYTES that the library holds on every GPU it runs on until the
+ * process ends (its address is looked up once per device, on the first call
+ * there). The call allocates nothing: no hipMalloc, hipFree or allocating
+ * library routine. Every call on one GPU uses that GPU's single array, and
+ * nothing in it has to start cleared: calls that overlap in time on one GPU
+ * (on different streams, or from different host threads without ordering)
+ * race on it and give undefined results; calls ordered on one stream are
+ * safe. The workspace these sizes need is rb_workspace_size's; sizes needing
+ * more than RB_SCRATCH_BYTES (for instance more than 64 requests of 768-d
+ * bf16 rows through the tile scan, whose worst-case candidate overflow area
+ * grows with the batch) are refused with RB_ERR_SCRATCH before anything is
+ * enqueued. Errors: those of rb_route_batch (RB_ERR_WORKSPACE aside), plus
+ * RB_ERR_SCRATCH, and RB_ERR_HIP if the array's address cannot be found. */
+rb_status rb_route_batch_noalloc(const void *queries, const void *bank, const float *bank_norms,
+                                 rb_dtype dtype, int B, int N, int d, int k,
+                                 const float *bank_qual, const float *bank_len, int M,
+                                 const int32_t *prompt_len, const rb_instances *inst, int I,
+                                 rb_weights w, int32_t *assign, float *chosen_score,
+                                 int32_t *nbr_idx, float *nbr_dist, float *q_hat, float *l_hat,
+                                 float *score0, void *stream);
 
 /* Carry the dead-reckoned state across a gap of dt_seconds between batches:
  *   prefill_q[i] = max(0, prefill_q[i] - prefill_rate[i]*dt)

@@ -21,17 +21,19 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "librouteb.so")
 
 RB_OK, RB_ERR_NULL, RB_ERR_DIMS, RB_ERR_DTYPE, RB_ERR_WEIGHTS = 0, -1, -2, -3, -4
-RB_ERR_WORKSPACE, RB_ERR_UNSUPPORTED, RB_ERR_HIP, RB_ERR_ALIGN = -5, -6, -7, -8
+RB_ERR_WORKSPACE, RB_ERR_UNSUPPORTED, RB_ERR_HIP, RB_ERR_ALIGN, RB_ERR_SCRATCH = -5, -6, -7, -8, -9
 RB_F32, RB_BF16 = 0, 1
 RB_KNN_UNIFORM, RB_KNN_INV_DIST = 0, 1
 RB_ORDER_ARRIVAL, RB_ORDER_LPT = 0, 1
 RB_FLAG_OVERLAP, RB_FLAG_LISTS_ONLY, RB_FLAG_FROM_LISTS = 1, 2, 4
 RB_MAX_K, RB_MAX_D, RB_MAX_I, RB_MAX_M = 64, 2048, 1024, 1024
+RB_SCRATCH_BYTES = 64 << 20
 
 # every symbol include/routebalance.h declares
 EXPORTS = ("rb_status_string", "rb_workspace_size", "rb_bank_norms", "rb_knn_topk", "rb_predict",
            "rb_score", "rb_assign", "rb_assign_ex", "rb_knn_predict", "rb_route_batch",
-           "rb_route_batch_ex", "rb_advance_state", "rb_profile_scan_events")
+           "rb_route_batch_ex", "rb_advance_state", "rb_profile_scan_events",
+           "rb_route_batch_noalloc")
 
 
 class RbError(RuntimeError):
@@ -81,6 +83,9 @@ def _load():
         "rb_route_batch_ex": ([P, P, P, i, i, i, i, i, P, P, i, P, ctypes.POINTER(rb_instances),
                                i, rb_weights, ctypes.POINTER(rb_options), P, P, P, P, P, P, P, P,
                                sz, P], st),
+        "rb_route_batch_noalloc": ([P, P, P, i, i, i, i, i, P, P, i, P,
+                                    ctypes.POINTER(rb_instances), i, rb_weights, P, P, P, P, P,
+                                    P, P, P], st),
         "rb_advance_state": ([ctypes.POINTER(rb_instances), i, ctypes.c_float, P], st),
         "rb_profile_scan_events": ([P, P], st),
     }
@@ -380,6 +385,31 @@ def rb_route_batch(queries, bank, bank_norms, k: int, bank_qual, bank_len, promp
                                _ptr(nbr_idx), _ptr(nbr_dist), _ptr(q_hat), _ptr(l_hat),
                                _ptr(score0), _ptr(ws), ws.numel(), _stream(stream)),
            "rb_route_batch")
+    return assign
+
+
+def rb_route_batch_noalloc(queries, bank, bank_norms, k: int, bank_qual, bank_len, prompt_len,
+                           inst: DeviceInstances, weights, assign: Optional[torch.Tensor] = None,
+                           chosen: Optional[torch.Tensor] = None,
+                           nbr_idx: Optional[torch.Tensor] = None,
+                           nbr_dist: Optional[torch.Tensor] = None,
+                           q_hat: Optional[torch.Tensor] = None,
+                           l_hat: Optional[torch.Tensor] = None, stream=None,
+                           score0: Optional[torch.Tensor] = None):
+    """rb_route_batch on the library's static per-GPU workspace (no device
+    allocation by the library; ``assign`` should be passed in by callers that
+    cannot allocate, since otherwise this wrapper allocates it)."""
+    B, N, d, M = _route_args(queries, bank, bank_norms, k, bank_qual, bank_len, prompt_len, inst,
+                             None, nbr_idx, nbr_dist, q_hat, l_hat, score0, chosen, assign)
+    if assign is None:
+        assign = torch.empty(B, dtype=torch.int32, device=queries.device)
+    s = inst.struct()
+    _check(_lib.rb_route_batch_noalloc(_ptr(queries), _ptr(bank), _ptr(bank_norms),
+                                       _dtype_code(bank), B, N, d, k, _ptr(bank_qual),
+                                       _ptr(bank_len), M, _ptr(prompt_len), ctypes.byref(s),
+                                       inst.I, _w(weights), _ptr(assign), _ptr(chosen),
+                                       _ptr(nbr_idx), _ptr(nbr_dist), _ptr(q_hat), _ptr(l_hat),
+                                       _ptr(score0), _stream(stream)), "rb_route_batch_noalloc")
     return assign
 
 

@@ -4,6 +4,7 @@
 #include <math.h>
 
 #include <atomic>
+#include <mutex>
 
 #include "../../include/routebalance.h"
 #include "kernels.hpp"
@@ -12,6 +13,33 @@ namespace {
 
 constexpr int MAX_DEVICES = 64;
 std::atomic<int> g_num_cu[MAX_DEVICES];
+
+// The workspace of rb_route_batch_noalloc: one copy on every device the
+// library runs on. In host code `scratch` names a host-side stand-in, not
+// the device array; its device address comes from hipGetSymbolAddress, once
+// per device, and only that address is ever handed to a kernel.
+static __device__ __align__(256) uint8_t scratch[RB_SCRATCH_BYTES];
+std::atomic<void *> g_scratch[MAX_DEVICES];
+std::mutex g_scratch_mu;
+
+// Device address of the current device's scratch array, or null.
+void *scratch_ptr()
+{
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= MAX_DEVICES)
+        return nullptr;
+    void *p = g_scratch[dev].load(std::memory_order_acquire);
+    if (p)
+        return p;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    p = g_scratch[dev].load(std::memory_order_relaxed);
+    if (!p) {
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p)
+            return nullptr;
+        g_scratch[dev].store(p, std::memory_order_release);
+    }
+    return p;
+}
 
 // Compute units of the current device (cached per device).
 int num_cu(int *out)
@@ -257,6 +285,9 @@ const char *rb_status_string(rb_status s)
     case RB_ERR_UNSUPPORTED: return "RB_ERR_UNSUPPORTED: option not implemented";
     case RB_ERR_HIP: return "RB_ERR_HIP: HIP runtime or launch failure";
     case RB_ERR_ALIGN: return "RB_ERR_ALIGN: pointer not aligned as required";
+    case RB_ERR_SCRATCH:
+        return "RB_ERR_SCRATCH: these sizes need more workspace than the library's static "
+               "RB_SCRATCH_BYTES";
     }
     return "unknown rb_status";
 }
@@ -466,6 +497,38 @@ rb_status rb_route_batch_ex(const void *queries, const void *bank, const float *
                        prompt_len, inst, I, w, opts ? opts : &k_default_opts, assign,
                        chosen_score, nbr_idx, nbr_dist, q_hat, l_hat, score0, ws, ws_bytes,
                        stream);
+}
+
+rb_status rb_route_batch_noalloc(const void *queries, const void *bank, const float *bank_norms,
+                                 rb_dtype dtype, int B, int N, int d, int k,
+                                 const float *bank_qual, const float *bank_len, int M,
+                                 const int32_t *prompt_len, const rb_instances *inst, int I,
+                                 rb_weights w, int32_t *assign, float *chosen_score,
+                                 int32_t *nbr_idx, float *nbr_dist, float *q_hat, float *l_hat,
+                                 float *score0, void *stream)
+{
+    // the size checks of rb_route_batch first, so that a too-large batch is
+    // refused as such and not as a short workspace
+    rb_status s = check_knn_dims(dtype, B, N, d, k);
+    if (s != RB_OK)
+        return s;
+    if (M < 1 || M > RB_MAX_M)
+        return RB_ERR_DIMS;
+    if (B == 0)
+        return route_batch(queries, bank, bank_norms, dtype, B, N, d, k, bank_qual, bank_len, M,
+                           prompt_len, inst, I, w, &k_default_opts, assign, chosen_score, nbr_idx,
+                           nbr_dist, q_hat, l_hat, score0, nullptr, 0, stream);
+    rb::KnnPlan p;
+    if ((s = plan(B, N, d, dtype, k, &p)) != RB_OK)
+        return s;
+    if (route_extra(p.bytes, B, k, M).bytes > (size_t)RB_SCRATCH_BYTES)
+        return RB_ERR_SCRATCH;
+    void *ws = scratch_ptr();
+    if (!ws)
+        return RB_ERR_HIP;
+    return route_batch(queries, bank, bank_norms, dtype, B, N, d, k, bank_qual, bank_len, M,
+                       prompt_len, inst, I, w, &k_default_opts, assign, chosen_score, nbr_idx,
+                       nbr_dist, q_hat, l_hat, score0, ws, RB_SCRATCH_BYTES, stream);
 }
 
 rb_status rb_profile_scan_events(void *begin, void *end)

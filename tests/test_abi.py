@@ -38,7 +38,7 @@ def test_header_declares_and_library_exports_every_entry_point():
 
 
 def test_status_strings():
-    for code in range(-8, 1):
+    for code in range(-9, 1):
         assert rb.rb_status_string(code).startswith("RB_")
     assert "unknown" in rb.rb_status_string(5)
 
