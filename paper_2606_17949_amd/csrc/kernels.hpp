@@ -34,17 +34,12 @@ constexpr int MERGE_CAP = 2048;     // candidates per query the merge holds in L
 constexpr int MERGE_MAX_LISTS = 64 * 64;   // 64 lists per lane
 constexpr int RB_MAX_K_DEV = 64;    // largest k (the ABI limit)
 constexpr int SEED_MAX_GROUPS = 2048;  // S / 16 for S <= 32768
-// The query-resident scan (a batch of at most RQ_WAVES*RQ_QW*16 queries of
-// RQ_NKS full k-steps, k <= RQ_MAX_K): RQ_WAVES waves of RQ_QW query groups,
-// blocks of RQ_ROWS bank rows, stages of RQ_KSTG k-steps of a block, a ring
-// of RQ_STAGES stages in LDS.
+// The query-resident scan (bf16 rows of 384, 512, 768 or 1024 elements, a
+// batch that fits its waves' registers): RQ_WAVES waves, blocks of RQ_ROWS
+// bank rows, a ring of stages of a block's k-steps in LDS.
 constexpr int RQ_WAVES = 8;
-constexpr int RQ_QW = 2;
 constexpr int RQ_ROWS = 32;
-constexpr int RQ_KSTG = 24;
-constexpr int RQ_STAGES = 2;
-constexpr int RQ_NKS = 24;
-constexpr int RQ_MAX_K = 16;
+constexpr int RQ_SMALL_B_MIN_ROWS = 2048;   // bank rows per compute unit, batches of <= 64
 
 // How one rb_knn_topk call is split (the tile scan; the query-resident scan
 // differs in that one workgroup holds the whole batch, so n_qt = 1).
@@ -58,10 +53,12 @@ constexpr int RQ_MAX_K = 16;
 //    workgroup per (chunk, tile); each of its SCAN_WAVES waves owns 16*rt rows per
 //    iteration; the workgroup keeps, per query, one list of the k best
 //    candidates that pass the bound.
-//  * merge: per query, the k smallest of its W = n_chunks lists.
+//  * merge: per query, the k smallest of its W lists (W = n_chunks, times
+//    the row halves rs of the query-resident scan).
 struct KnnPlan {
     int kind;           // 0 tile scan, 1 query-resident scan
-    int qw;             // query groups per wave of the query-resident scan
+    int qw, rs, spb;    // query-resident scan: query groups per wave, row halves, stages per block,
+    int stages;         //   ring slots
     int dtype;          // 0 fp32, 1 bf16
     int B, N, d, k;
     int nks, nksp;      // 64-byte k-steps per row, padded to SCAN_KPAD

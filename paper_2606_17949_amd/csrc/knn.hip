@@ -511,14 +511,62 @@ int plan_knn(int B, int N, int d, int dtype, int k, int num_cu, KnnPlan *p, int 
     p->nks = (d + 4 * vec - 1) / (4 * vec);
     p->nksp = (p->nks + SCAN_KPAD - 1) / SCAN_KPAD * SCAN_KPAD;
     const bool ragged = d % (4 * vec) != 0;
-    // a batch of 65..256 queries of bf16 rows of RQ_NKS full k-steps stays in
-    // the registers of one workgroup; smaller batches fit the tile scan's LDS
-    // whole
-    p->kind = dtype == 1 && !ragged && p->nks == RQ_NKS && B > 64 &&
-                      B <= RQ_WAVES * RQ_QW * 16 && k <= RQ_MAX_K
-                  ? 1
-                  : 0;
-    p->qw = p->kind == 1 ? RQ_QW : 0;
+    // The query-resident scan takes bf16 rows of 12, 16, 24 or 32 full
+    // k-steps (d = 384, 512, 768, 1024) when the batch fits the registers of
+    // one workgroup: the first (query groups per wave, row halves) of the
+    // row length's list, in order of capacity, that holds B queries, with
+    // the first ring whose LDS (ring, lists, query data) fits: four slots of
+    // half blocks (whole blocks for d = 384), which keep three stages of
+    // loads in flight, else two slots of whole or of half blocks. A wave
+    // holds qw * nks * 4 registers of query fragments, at most 192. A batch
+    // of up to 64 queries takes it only over a bank of at least
+    // RQ_SMALL_B_MIN_ROWS rows per compute unit: over fewer, its per-workgroup
+    // start (every wave loading its queries, the ring filling) costs more than
+    // the tile scan's, whose query tile stays in LDS (measured: 100,000 rows
+    // of 768 at 64 queries, 49.9 against 43.6 us cold; 1,000,000 rows, 264
+    // against 286 us).
+    p->kind = 0;
+    p->qw = p->rs = p->spb = p->stages = 0;
+    const bool rq_small_ok = (long)N >= (long)RQ_SMALL_B_MIN_ROWS * num_cu;
+    if (dtype == 1 && !ragged && B >= 1 && (B > 64 || rq_small_ok)) {
+        static const int tab12[][2] = {{1, 2}, {2, 2}, {4, 2}};
+        static const int tab16[][2] = {{1, 2}, {2, 2}, {2, 1}};
+        static const int tab32[][2] = {{1, 2}, {1, 1}};
+        const int(*tab)[2] = nullptr;
+        int n_tab = 0;
+        if (p->nks == 12) {
+            tab = tab12;
+            n_tab = 3;
+        } else if (p->nks == 16 || p->nks == 24) {
+            tab = tab16;
+            n_tab = 3;
+        } else if (p->nks == 32) {
+            tab = tab32;
+            n_tab = 2;
+        }
+        for (int t = 0; t < n_tab && p->kind == 0; ++t) {
+            const int qw = tab[t][0], rs = tab[t][1];
+            if ((RQ_WAVES / rs) * qw * 16 < B)
+                continue;
+            // (stages per block, slots)
+            static const int ring12[][2] = {{1, 4}, {1, 2}};
+            static const int ring16[][2] = {{2, 4}, {1, 2}, {2, 2}};
+            static const int ring32[][2] = {{2, 4}, {2, 2}};
+            const int(*ring)[2] = p->nks == 12 ? ring12 : p->nks == 32 ? ring32 : ring16;
+            const int n_ring = p->nks == 16 || p->nks == 24 ? 3 : 2;
+            for (int u = 0; u < n_ring; ++u) {
+                const int spb = ring[u][0], stages = ring[u][1];
+                if (rq_layout(k, qw, p->nks / spb, stages).bytes <= LDS_LIMIT) {
+                    p->kind = 1;
+                    p->qw = qw;
+                    p->rs = rs;
+                    p->spb = spb;
+                    p->stages = stages;
+                    break;
+                }
+            }
+        }
+    }
     // tile scan: largest query tile that B can fill and whose lists fit in
     // LDS; then as many of its query groups resident in LDS as the rest of
     // the space holds
@@ -554,7 +602,7 @@ int plan_knn(int B, int N, int d, int dtype, int k, int num_cu, KnnPlan *p, int 
     p->n_qt = B > 0 ? (B + bm - 1) / bm : 1;
     if (p->kind == 1) {
         p->n_qt = 1;
-        p->lds_bytes = rq_layout(k, p->qw).bytes;
+        p->lds_bytes = rq_layout(k, p->qw, p->nks / p->spb, p->stages).bytes;
     }
     // one workgroup per compute unit (the LDS use allows no more); with
     // `reserve`, that many units of each XCD stay free: workgroups go to the
@@ -583,7 +631,7 @@ int plan_knn(int B, int N, int d, int dtype, int k, int num_cu, KnnPlan *p, int 
     }
     p->rows_per_chunk = rpc;
     p->n_chunks = (int)(((long)N + rpc - 1) / rpc);
-    p->W = p->n_chunks;
+    p->W = p->n_chunks * (p->kind == 1 ? p->rs : 1);
     if (p->W > MERGE_MAX_LISTS)
         return -1;
     // seed sample: about N/32 rows, 2048..32768, a multiple of 64 and at most N

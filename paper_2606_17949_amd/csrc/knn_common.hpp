@@ -65,14 +65,14 @@ struct RqLayout {
     uint32_t ring, norms, lists, qinfo, bytes;
 };
 
-__host__ __device__ inline RqLayout rq_layout(int k, int qw)
+__host__ __device__ inline RqLayout rq_layout(int k, int qw, int kstg, int stages)
 {
     RqLayout L;
     uint32_t o = 0;
-    L.ring = o;    // [RQ_STAGES][RQ_KSTG * RQ_ROWS / 16][64] bank fragments
-    o += (uint32_t)RQ_STAGES * RQ_KSTG * (RQ_ROWS / 16) * WAVE * 16;
-    L.norms = o;   // [RQ_STAGES][64] |x|^2 of the rows of a block (with its first stage)
-    o += (uint32_t)RQ_STAGES * WAVE * 4;
+    L.ring = o;    // [stages][kstg * RQ_ROWS / 16][64] bank fragments
+    o += (uint32_t)stages * kstg * (RQ_ROWS / 16) * WAVE * 16;
+    L.norms = o;   // [stages][64] |x|^2 of the rows of a block (with its first stage)
+    o += (uint32_t)stages * WAVE * 4;
     L.lists = o;   // [waves][16 * qw][k] (key << 32 | index), one list per owned query
     o += (uint32_t)RQ_WAVES * qw * 16 * k * 8;
     L.qinfo = o;   // [waves][16 * qw] |q|^2, then [waves][16 * qw] the shared bound
@@ -82,9 +82,13 @@ __host__ __device__ inline RqLayout rq_layout(int k, int qw)
 }
 
 // The bank-scan launchers, one translation unit per element type and
-// k-step raggedness (they are the bulk of the compile time), and one for the
-// query-resident scan.
+// k-step raggedness (they are the bulk of the compile time), and one per row
+// length for the query-resident scan.
 hipError_t launch_scan_rq(const KnnPlan &p, const ScanArgs &a, hipStream_t s);
+hipError_t launch_scan_rq12(const KnnPlan &p, const ScanArgs &a, hipStream_t s);
+hipError_t launch_scan_rq16(const KnnPlan &p, const ScanArgs &a, hipStream_t s);
+hipError_t launch_scan_rq24(const KnnPlan &p, const ScanArgs &a, hipStream_t s);
+hipError_t launch_scan_rq32(const KnnPlan &p, const ScanArgs &a, hipStream_t s);
 hipError_t launch_scan_bf16(const KnnPlan &p, const ScanArgs &a, hipStream_t s);
 hipError_t launch_scan_bf16_ragged(const KnnPlan &p, const ScanArgs &a, hipStream_t s);
 hipError_t launch_scan_f32(const KnnPlan &p, const ScanArgs &a, hipStream_t s);

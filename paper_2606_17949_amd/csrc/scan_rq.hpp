@@ -1,7 +1,7 @@
 // The bank scan of the exact k-nearest-neighbour search (RouteBalance Sec. 4.2:
 // the KNN lookup of Alg. 1) for a batch whose whole query tile fits in the
 // registers of one workgroup: bf16 rows of NKS full k-steps, at most
-// RQ_WAVES * QW * 16 queries.
+// (RQ_WAVES / RS) * QW * 16 queries.
 #pragma once
 
 #include "knn_common.hpp"
@@ -17,30 +17,52 @@ __device__ __forceinline__ void dma4(__amdgpu_buffer_rsrc_t r, float *dst, uint3
                                              (int)voffset, 0, 0, 0);
 }
 
-// One workgroup per bank chunk; RQ_WAVES waves, two per SIMD. Wave w owns
-// queries [16*QW*w, 16*QW*(w+1)) and
-// holds their fragments for every k-step in registers for the whole kernel,
-// so no query byte is loaded twice. The chunk goes by in blocks of RQ_ROWS
-// rows; each block's k-steps are cut into
-// stages of RQ_KSTG k-steps, which global-to-LDS loads bring into a ring of
-// RQ_STAGES slots, RQ_STAGES - 1 stages ahead of the MFMAs, so that every
-// bank byte crosses from L2 into the compute unit once and serves all the
-// waves. Each wave keeps, per owned query, its own list of the k best
-// candidates of the chunk (no other wave touches it) and its own candidate
-// threshold; the lists start from the shared bound the seed pass computed.
-template <int NKS, int QW>
+// Bank fragments travel from HBM to LDS in whole 128-byte lines: one
+// global-to-LDS load brings 8 rows x 128 bytes (two k-steps of each row,
+// eight 16-byte chunks of one line per group of 8 lanes), so every line is
+// fetched by one instruction. In LDS, load f of a stage (row group
+// rg = f % 4 of the block, k-step pair f / 4) holds row rg*8 + ri's chunk c
+// (quarter c % 4 of k-step 2*(f/4) + c/4) at position 8*ri + (c ^ ri ^ (rg & 1)).
+// The XOR spreads the 16 rows of a tile over distinct LDS bank groups, so
+// the MFMA A-fragment read (lane (col, jg): row col, quarter jg of one
+// k-step) is conflict free.
+__device__ __forceinline__ uint32_t rq_chunk(int ri, int rg, int c)
+{
+    return (uint32_t)(8 * ri + (c ^ ri ^ (rg & 1)));
+}
+
+// One workgroup per bank chunk; RQ_WAVES waves, two per SIMD, in RS row
+// halves of RQ_WAVES / RS query slots. Wave w owns the queries of slot
+// w % (RQ_WAVES / RS), [16*QW*slot, 16*QW*(slot+1)), and holds their
+// fragments for every k-step in registers for the whole kernel, so no query
+// byte is loaded twice. The chunk goes by in blocks of RQ_ROWS rows (two
+// 16-row MFMA tiles); with RS = 1 every wave takes both tiles of a block,
+// with RS = 2 the waves of row half h take tile h (so a batch of up to 64
+// requests still keeps all eight waves busy). Each block's k-steps are cut
+// into SPB stages, which global-to-LDS loads bring in whole 128-byte lines
+// into a ring of S slots, S - 1 stages ahead of the MFMAs, so
+// that every bank byte crosses from L2 into the compute unit once and serves
+// all the waves. Each wave keeps, per owned query, its own list of the k
+// best candidates of its rows of the chunk (no other wave touches it) and its
+// own candidate threshold; the lists start from the shared bound the seed
+// pass computed. A chunk therefore leaves RS lists per query.
+template <int NKS, int QW, int RS, int SPB, int S>
 __global__ __launch_bounds__(RQ_WAVES * WAVE, 1) void rq_scan_kernel(const ScanArgs A)
 {
-    constexpr int TT = RQ_ROWS / 16, KSTG = RQ_KSTG, S = RQ_STAGES;
+    constexpr int TT = RQ_ROWS / 16;
+    constexpr int KSTG = NKS / SPB;             // k-steps of one stage
     constexpr int F = KSTG * TT;                // fragments of one stage
     constexpr int FPW = F / RQ_WAVES;           // of them, loaded by each wave
-    constexpr int SPB = NKS / KSTG;             // stages of one block
     constexpr int QPW = QW * 16;                // queries of one wave
-    static_assert(NKS % KSTG == 0 && F % RQ_WAVES == 0, "whole stages, equal shares");
+    constexpr int NQS = RQ_WAVES / RS;          // query slots
+    constexpr int TW = TT / RS;                 // tiles of a block each wave takes
+    static_assert(NKS % SPB == 0 && F % RQ_WAVES == 0, "whole stages, equal shares");
+    static_assert(KSTG % 2 == 0 && TT == 2, "stages of whole k-step pairs, 32-row blocks");
+    static_assert(RS == 1 || RS == 2, "one or two row halves");
     static_assert(RQ_ROWS <= WAVE, "one norm per lane");
 
     extern __shared__ __align__(16) uint8_t smem[];
-    const RqLayout L = rq_layout(A.k, QW);
+    const RqLayout L = rq_layout(A.k, QW, KSTG, S);
     i32x4 *ring = (i32x4 *)(smem + L.ring);              // [S][F][64] fragments
     float *nslot = (float *)(smem + L.norms);            // [S][64] |x|^2 of a block's rows
     uint64_t *lists = (uint64_t *)(smem + L.lists);      // [waves][QPW][k]
@@ -53,6 +75,7 @@ __global__ __launch_bounds__(RQ_WAVES * WAVE, 1) void rq_scan_kernel(const ScanA
     const int tid = threadIdx.x, lane = tid & 63;
     __builtin_assume(tid < RQ_WAVES * WAVE);
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int slot_q = wave % NQS, half = wave / NQS;   // query slot, row half
     const int col = lane & 15, jg = lane >> 4;
     const int k = A.k;
     const uint32_t rowb = (uint32_t)A.d * 2;
@@ -61,7 +84,7 @@ __global__ __launch_bounds__(RQ_WAVES * WAVE, 1) void rq_scan_kernel(const ScanA
     const int nrows = rend > rbeg ? (int)(rend - rbeg) : 0;
     const int n_blk = (nrows + RQ_ROWS - 1) / RQ_ROWS;
     const int n_stg = n_blk * SPB;
-    const int qw0 = wave * QPW;
+    const int qw0 = slot_q * QPW;
     const bool active = qw0 < A.B;   // (a wave past the batch only loads its share)
 
     // ---- the wave's queries: fragments of every k-step (zero past the batch)
@@ -79,10 +102,10 @@ __global__ __launch_bounds__(RQ_WAVES * WAVE, 1) void rq_scan_kernel(const ScanA
     // LDS (they are needed only for candidates)
     float *qn_w = qn_l + wave * QPW;
     uint32_t *tau_w = tau_l + wave * QPW;
-    if (lane < QPW) {
-        const int q = qw0 + lane;
-        qn_w[lane] = q < A.B ? A.qn[q] : 0.f;
-        tau_w[lane] = q < A.B ? A.tau[q] : KEY_NONE;
+    for (int i = lane; i < QPW; i += WAVE) {
+        const int q = qw0 + i;
+        qn_w[i] = q < A.B ? A.qn[q] : 0.f;
+        tau_w[i] = q < A.B ? A.tau[q] : KEY_NONE;
     }
     // Filter threshold on the accumulators for bound key tk: a value is a
     // candidate if acc >= nu (a superset of distance <= the bound).
@@ -114,6 +137,10 @@ __global__ __launch_bounds__(RQ_WAVES * WAVE, 1) void rq_scan_kernel(const ScanA
         make_rsrc(A.bank + (size_t)rbeg * rowb, (uint32_t)nrows * rowb);
     const __amdgpu_buffer_rsrc_t rnm = make_rsrc(A.bank_norms + rbeg, (uint32_t)nrows * 4u);
     const __amdgpu_buffer_rsrc_t rnone = make_rsrc(A.bank, 0u);
+    // this lane's place in a load: row ri of the row group, the chunk of the
+    // 128-byte line that lands at its position (rq_chunk inverted)
+    const int dri = lane >> 3;
+    auto dma_chunk = [&](int rg) { return (lane & 7) ^ dri ^ (rg & 1); };
     auto issue = [&](int z) {
         const int slot = z % S, bz = z / SPB, st = z - bz * SPB;
         const bool real = z < n_stg;
@@ -121,9 +148,9 @@ __global__ __launch_bounds__(RQ_WAVES * WAVE, 1) void rq_scan_kernel(const ScanA
 #pragma unroll
         for (int j = 0; j < FPW; ++j) {
             const int f = wave + RQ_WAVES * j;
-            const int t = f % TT, ks = st * KSTG + f / TT;
-            const uint32_t vo =
-                (uint32_t)(bz * RQ_ROWS + t * 16 + col) * rowb + ks * KSTEP_BYTES + jg * 16;
+            const int rg = f % 4, pair = st * (KSTG / 2) + f / 4;
+            const uint32_t vo = (uint32_t)(bz * RQ_ROWS + rg * 8 + dri) * rowb +
+                                pair * (2 * KSTEP_BYTES) + dma_chunk(rg) * 16;
             dma16(r, ring + (slot * F + f) * WAVE, vo);
         }
         if (st == 0 && wave == RQ_WAVES - 1)
@@ -168,7 +195,7 @@ __global__ __launch_bounds__(RQ_WAVES * WAVE, 1) void rq_scan_kernel(const ScanA
 
     int z = 0;   // the stage being consumed
     for (int b = 0; b < n_blk; ++b) {
-        f32x4 acc[TT][QW];
+        f32x4 acc[TW][QW];
         static_for<0, SPB>([&](auto ST) {
             constexpr int st = decltype(ST)::value;
             // this wave's part of stage z has landed once at most FPW*(S-2)
@@ -186,39 +213,51 @@ __global__ __launch_bounds__(RQ_WAVES * WAVE, 1) void rq_scan_kernel(const ScanA
                 // the accumulators start from -|x|^2/2 of their rows (-inf
                 // for rows past the chunk)
 #pragma unroll
-                for (int t = 0; t < TT; ++t) {
-                    const f32x4 xn = *(const f32x4 *)(nslot + slot * WAVE + t * 16 + jg * 4);
+                for (int t = 0; t < TW; ++t) {
+                    const int tt = RS == 2 ? half : t;
+                    const f32x4 xn = *(const f32x4 *)(nslot + slot * WAVE + tt * 16 + jg * 4);
                     f32x4 h;
 #pragma unroll
                     for (int e = 0; e < 4; ++e)
-                        h[e] = b * RQ_ROWS + t * 16 + jg * 4 + e < nrows ? -0.5f * xn[e]
-                                                                        : -INFINITY;
+                        h[e] = b * RQ_ROWS + tt * 16 + jg * 4 + e < nrows ? -0.5f * xn[e]
+                                                                         : -INFINITY;
 #pragma unroll
                     for (int g = 0; g < QW; ++g)
                         acc[t][g] = h;
                 }
             }
             if (active) {
-                const i32x4 *fr = ring + slot * F * WAVE + lane;
+                // the lane's A fragment of tile tt, k-step j of the stage: row
+                // col of the tile, quarter jg, at load (j/2)*4 + rg
+                const i32x4 *fr = ring + slot * F * WAVE;
+                uint32_t fbase[TW][2];
+#pragma unroll
+                for (int t = 0; t < TW; ++t) {
+                    const int tt = RS == 2 ? half : t;
+                    const int ri = col & 7, rg = tt * 2 + (col >> 3);
+#pragma unroll
+                    for (int h = 0; h < 2; ++h)
+                        fbase[t][h] = (uint32_t)rg * WAVE + rq_chunk(ri, rg, 4 * h + jg);
+                }
                 static_for<0, KSTG>([&](auto J) {
                     constexpr int j = decltype(J)::value, s = st * KSTG + j;
-                    i32x4 a[TT];
+                    i32x4 a[TW];
 #pragma unroll
-                    for (int t = 0; t < TT; ++t)
-                        a[t] = fr[(j * TT + t) * WAVE];
+                    for (int t = 0; t < TW; ++t)
+                        a[t] = fr[(j / 2) * 4 * WAVE + fbase[t][j & 1]];
 #pragma unroll
-                    for (int t = 0; t < TT; ++t)
+                    for (int t = 0; t < TW; ++t)
 #pragma unroll
                         for (int g = 0; g < QW; ++g)
                             acc[t][g] = mfma_step<1>(a[t], qf[g][s], acc[t][g]);
                 });
                 // two k-steps of fragment reads in flight: the reads of k-steps
                 // 0 and 1, then per k-step its MFMAs and the reads two ahead
-                __builtin_amdgcn_sched_group_barrier(0x100, 2 * TT, 0);
+                __builtin_amdgcn_sched_group_barrier(0x100, 2 * TW, 0);
                 static_for<0, KSTG>([&](auto J) {
-                    __builtin_amdgcn_sched_group_barrier(0x008, TT * QW, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x008, TW * QW, 0);
                     if constexpr (decltype(J)::value + 2 < KSTG)
-                        __builtin_amdgcn_sched_group_barrier(0x100, TT, 0);
+                        __builtin_amdgcn_sched_group_barrier(0x100, TW, 0);
                 });
             }
             ++z;
@@ -231,20 +270,21 @@ __global__ __launch_bounds__(RQ_WAVES * WAVE, 1) void rq_scan_kernel(const ScanA
             constexpr int g = decltype(G)::value;
             float m = -INFINITY;
 #pragma unroll
-            for (int t = 0; t < TT; ++t)
+            for (int t = 0; t < TW; ++t)
                 m = fmaxf(m, fmaxf(fmaxf(acc[t][g][0], acc[t][g][1]),
                                    fmaxf(acc[t][g][2], acc[t][g][3])));
             if (!ballot(m >= nu[g]))
                 return;
             const float qg = qn_w[g * 16 + col];
 #pragma unroll
-            for (int t = 0; t < TT; ++t)
+            for (int t = 0; t < TW; ++t) {
+                const int tt = RS == 2 ? half : t;
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     const float a = acc[t][g][e];
                     uint64_t mk = ballot(a >= nu[g]);
                     const uint32_t key = f2key(fmaf(-2.f, a, qg));
-                    const int32_t idx = (int32_t)(rbeg + b * RQ_ROWS + t * 16 + jg * 4 + e);
+                    const int32_t idx = (int32_t)(rbeg + b * RQ_ROWS + tt * 16 + jg * 4 + e);
                     while (mk) {
                         const int src = __builtin_ctzll(mk);
                         mk &= mk - 1;
@@ -252,14 +292,17 @@ __global__ __launch_bounds__(RQ_WAVES * WAVE, 1) void rq_scan_kernel(const ScanA
                                __builtin_amdgcn_readlane(idx, src));
                     }
                 }
+            }
         });
     }
 
-    // ---- the wave's lists -> workspace [B][n_chunks][k], valid entries first
-    // (no global-to-LDS load may still be in flight when the workgroup ends)
+    // ---- the wave's lists -> workspace [B][n_chunks * RS][k], list c*RS + half
+    // of each query, valid entries first (no global-to-LDS load may still be
+    // in flight when the workgroup ends)
     wait_vmcnt<0>();
     if (!active)
         return;
+    const int W = A.n_chunks * RS;
     for (int i = 0; i < QPW; ++i) {
         const int q = qw0 + i;
         if (q >= A.B)
@@ -268,7 +311,7 @@ __global__ __launch_bounds__(RQ_WAVES * WAVE, 1) void rq_scan_kernel(const ScanA
         const uint32_t key = (uint32_t)(v >> 32);
         const bool valid = key != KEY_NONE;
         const uint64_t m = ballot(valid);
-        const size_t o = (size_t)q * A.n_chunks + c;
+        const size_t o = (size_t)q * W + c * RS + half;
         if (valid) {
             const int pos = mbcnt(m);
             A.ckey[o * k + pos] = key;
@@ -279,16 +322,59 @@ __global__ __launch_bounds__(RQ_WAVES * WAVE, 1) void rq_scan_kernel(const ScanA
     }
 }
 
-template <int NKS, int QW>
+template <int NKS, int QW, int RS, int SPB, int S>
 hipError_t launch_rq_scan(const ScanArgs &a, size_t lds, int grid, hipStream_t s)
 {
-    auto kern = rq_scan_kernel<NKS, QW>;
+    auto kern = rq_scan_kernel<NKS, QW, RS, SPB, S>;
     hipError_t e = hipFuncSetAttribute((const void *)kern,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess)
         return e;
     hipLaunchKernelGGL(kern, dim3(grid), dim3(RQ_WAVES * WAVE), lds, s, a);
     return hipGetLastError();
+}
+
+// The instantiations of one row length: the (QW, RS) and (SPB, S) the plan
+// may choose for it (plan_knn's tables; QW * NKS * 4 registers of query
+// fragments stay within 192).
+template <int NKS, int QW, int RS>
+hipError_t launch_rq_stages(const KnnPlan &p, const ScanArgs &a, hipStream_t s)
+{
+    if constexpr (NKS == 12) {
+        if (p.spb == 1 && p.stages == 4)
+            return launch_rq_scan<NKS, QW, RS, 1, 4>(a, p.lds_bytes, p.grid, s);
+    } else {
+        if (p.spb == 2 && p.stages == 4)
+            return launch_rq_scan<NKS, QW, RS, 2, 4>(a, p.lds_bytes, p.grid, s);
+        if (p.spb == 2 && p.stages == 2)
+            return launch_rq_scan<NKS, QW, RS, 2, 2>(a, p.lds_bytes, p.grid, s);
+    }
+    if constexpr (NKS != 32)
+        if (p.spb == 1 && p.stages == 2)
+            return launch_rq_scan<NKS, QW, RS, 1, 2>(a, p.lds_bytes, p.grid, s);
+    return hipErrorInvalidValue;
+}
+
+template <int NKS>
+hipError_t launch_rq_nks(const KnnPlan &p, const ScanArgs &a, hipStream_t s)
+{
+#define RB_RQ(QW_, RS_)                                                                          \
+    if (p.qw == QW_ && p.rs == RS_)                                                             \
+        return launch_rq_stages<NKS, QW_, RS_>(p, a, s);
+    if constexpr (NKS == 12) {
+        RB_RQ(1, 2)
+        RB_RQ(2, 2)
+        RB_RQ(4, 2)
+    } else if constexpr (NKS == 16 || NKS == 24) {
+        RB_RQ(1, 2)
+        RB_RQ(2, 2)
+        RB_RQ(2, 1)
+    } else if constexpr (NKS == 32) {
+        RB_RQ(1, 2)
+        RB_RQ(1, 1)
+    }
+#undef RB_RQ
+    return hipErrorInvalidValue;
 }
 
 }  // namespace

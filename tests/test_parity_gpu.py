@@ -89,15 +89,32 @@ KNN_CASES = [
     # the seed bound's wave holds each lane's two smallest group minima
     ("bf16", 100, 700, 768, 20),    # 40 groups: fewer than the wave's lanes
     ("bf16", 100, 1600, 768, 64),   # 100 groups, one or two per lane, largest k
-    # batches of 65..256 requests with d = 768 take the query-resident scan
-    ("bf16", 100, 50000, 768, 10),  # a partly filled wave and idle waves
-    ("bf16", 200, 100003, 768, 16), # its largest k; chunks that end inside a block
+    # bf16 rows of 384, 512, 768 or 1024 elements take the query-resident
+    # scan while the batch fits its registers: (query groups per wave, row
+    # halves) of (1, 2) up to 64 requests, (2, 2) up to 128, then (4, 2) for
+    # d = 384 and (2, 1) for d = 512 and 768 up to 256
+    ("bf16", 100, 50000, 768, 10),  # (2, 2): a partly filled wave and idle waves
+    ("bf16", 200, 100003, 768, 16), # (2, 1); chunks that end inside a block
     ("bf16", 129, 70000, 768, 1),   # k = 1
-    ("bf16", 200, 9000, 768, 17),   # k past its limit: the tile scan again
+    ("bf16", 200, 9000, 768, 17),
     ("bf16", 70, 20, 768, 10),      # fewer bank rows than one of its 32-row blocks
-    ("bf16", 65, 1, 768, 1),        # its smallest batch, a single bank row
+    ("bf16", 65, 1, 768, 1),        # a single bank row
     ("bf16", 256, 600, 768, 10),    # a full batch with a 36-group seed
     ("bf16", 200, 4096, 768, 16),   # 128 seed groups: exactly two per lane of the bound
+    ("bf16", 1, 530000, 768, 10),   # a single request: two active waves
+    ("bf16", 64, 530000, 768, 64),  # (1, 2), k = 64 (batches of up to 64 take it from
+                                    # 2,048 rows per compute unit)
+    ("bf16", 90, 60000, 768, 20),   # (2, 2), k = 20
+    ("bf16", 40, 530000, 384, 10),  # d = 384, (1, 2)
+    ("bf16", 40, 30000, 384, 10),   # the same batch over a small bank: the tile scan
+    ("bf16", 100, 30000, 384, 20),  # d = 384, (2, 2), k = 20
+    ("bf16", 256, 50000, 384, 10),  # d = 384, (4, 2)
+    ("bf16", 64, 530000, 512, 64),  # d = 512, (1, 2), k = 64
+    ("bf16", 128, 40000, 512, 20),  # d = 512, (2, 2)
+    ("bf16", 250, 40000, 512, 10),  # d = 512, (2, 1)
+    ("bf16", 64, 530000, 1024, 10), # d = 1024, (1, 2)
+    ("bf16", 128, 30000, 1024, 64), # d = 1024, (1, 1), k = 64: half-block stages
+    ("bf16", 100, 40, 1024, 33),    # fewer rows than chunks
 ]
 
 
