@@ -529,14 +529,14 @@ int plan_knn(int B, int N, int d, int dtype, int k, int num_cu, KnnPlan *p, int 
     p->qw = p->rs = p->spb = p->stages = 0;
     const bool rq_small_ok = (long)N >= (long)RQ_SMALL_B_MIN_ROWS * num_cu;
     if (dtype == 1 && !ragged && B >= 1 && (B > 64 || rq_small_ok)) {
-        static const int tab12[][2] = {{1, 2}, {2, 2}, {4, 2}};
+        static const int tab12[][2] = {{1, 2}, {2, 2}, {4, 2}, {4, 1}};
         static const int tab16[][2] = {{1, 2}, {2, 2}, {2, 1}};
         static const int tab32[][2] = {{1, 2}, {1, 1}};
         const int(*tab)[2] = nullptr;
         int n_tab = 0;
         if (p->nks == 12) {
             tab = tab12;
-            n_tab = 3;
+            n_tab = 4;
         } else if (p->nks == 16 || p->nks == 24) {
             tab = tab16;
             n_tab = 3;

@@ -58,6 +58,12 @@ __global__ __launch_bounds__(RQ_WAVES * WAVE, 1) void rq_scan_kernel(const ScanA
     constexpr int TW = TT / RS;                 // tiles of a block each wave takes
     static_assert(NKS % SPB == 0 && F % RQ_WAVES == 0, "whole stages, equal shares");
     static_assert(KSTG % 2 == 0 && TT == 2, "stages of whole k-step pairs, 32-row blocks");
+    // With four query groups a wave holds 192 registers of query fragments;
+    // both tiles' accumulators would not fit beside them, so such a wave
+    // takes the tiles of a block one after the other (one stage per block)
+    constexpr bool TSEQ = QW >= 4 && TW == 2;
+    constexpr int TA = TSEQ ? 1 : TW;           // tiles whose accumulators are live together
+    static_assert(!TSEQ || SPB == 1, "tiles one after the other within one stage");
     static_assert(RS == 1 || RS == 2, "one or two row halves");
     static_assert(RQ_ROWS <= WAVE, "one norm per lane");
 
@@ -193,95 +199,79 @@ __global__ __launch_bounds__(RQ_WAVES * WAVE, 1) void rq_scan_kernel(const ScanA
     }
     __syncthreads();
 
-    int z = 0;   // the stage being consumed
-    for (int b = 0; b < n_blk; ++b) {
-        f32x4 acc[TW][QW];
-        static_for<0, SPB>([&](auto ST) {
-            constexpr int st = decltype(ST)::value;
-            // this wave's part of stage z has landed once at most FPW*(S-2)
-            // loads are outstanding (the fragment loads of the S-2 stages
-            // issued after it); the barrier then tells that every wave's
-            // part has and that every wave is done with stage z - 1, whose
-            // slot the next load reuses
-            __builtin_amdgcn_sched_barrier(0);
-            wait_vmcnt<FPW * (S - 2)>();
-            stream_barrier();
-            issue(z + S - 1);
-            __builtin_amdgcn_sched_barrier(0);
-            const int slot = z % S;
-            if constexpr (st == 0) {
-                // the accumulators start from -|x|^2/2 of their rows (-inf
-                // for rows past the chunk)
+    // the block tile of wave tile t
+    auto tile_of = [&](int t) { return RS == 2 ? half : t; };
+    // accumulators of wave tiles t0 .. t0+TA-1 from -|x|^2/2 of their rows
+    // (-inf for rows past the chunk), the norms of block b in norm slot `slot`
+    auto init_acc = [&](f32x4(&ac)[TA][QW], int slot, int b, int t0) {
 #pragma unroll
-                for (int t = 0; t < TW; ++t) {
-                    const int tt = RS == 2 ? half : t;
-                    const f32x4 xn = *(const f32x4 *)(nslot + slot * WAVE + tt * 16 + jg * 4);
-                    f32x4 h;
+        for (int t = 0; t < TA; ++t) {
+            const int tt = tile_of(t0 + t);
+            const f32x4 xn = *(const f32x4 *)(nslot + slot * WAVE + tt * 16 + jg * 4);
+            f32x4 h;
 #pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        h[e] = b * RQ_ROWS + tt * 16 + jg * 4 + e < nrows ? -0.5f * xn[e]
-                                                                         : -INFINITY;
+            for (int e = 0; e < 4; ++e)
+                h[e] = b * RQ_ROWS + tt * 16 + jg * 4 + e < nrows ? -0.5f * xn[e] : -INFINITY;
 #pragma unroll
-                    for (int g = 0; g < QW; ++g)
-                        acc[t][g] = h;
-                }
-            }
-            if (active) {
-                // the lane's A fragment of tile tt, k-step j of the stage: row
-                // col of the tile, quarter jg, at load (j/2)*4 + rg
-                const i32x4 *fr = ring + slot * F * WAVE;
-                uint32_t fbase[TW][2];
+            for (int g = 0; g < QW; ++g)
+                ac[t][g] = h;
+        }
+    };
+    // the MFMAs of stage ST (in slot `slot`) for wave tiles t0 .. t0+TA-1
+    auto mfma_tiles = [&](auto ST, f32x4(&ac)[TA][QW], int slot, int t0) {
+        constexpr int st = decltype(ST)::value;
+        // the lane's A fragment of tile tt, k-step j of the stage: row col of
+        // the tile, quarter jg, at load (j/2)*4 + rg
+        const i32x4 *fr = ring + slot * F * WAVE;
+        uint32_t fbase[TA][2];
 #pragma unroll
-                for (int t = 0; t < TW; ++t) {
-                    const int tt = RS == 2 ? half : t;
-                    const int ri = col & 7, rg = tt * 2 + (col >> 3);
+        for (int t = 0; t < TA; ++t) {
+            const int tt = tile_of(t0 + t);
+            const int ri = col & 7, rg = tt * 2 + (col >> 3);
 #pragma unroll
-                    for (int h = 0; h < 2; ++h)
-                        fbase[t][h] = (uint32_t)rg * WAVE + rq_chunk(ri, rg, 4 * h + jg);
-                }
-                static_for<0, KSTG>([&](auto J) {
-                    constexpr int j = decltype(J)::value, s = st * KSTG + j;
-                    i32x4 a[TW];
+            for (int h = 0; h < 2; ++h)
+                fbase[t][h] = (uint32_t)rg * WAVE + rq_chunk(ri, rg, 4 * h + jg);
+        }
+        static_for<0, KSTG>([&](auto J) {
+            constexpr int j = decltype(J)::value, s = st * KSTG + j;
+            i32x4 a[TA];
 #pragma unroll
-                    for (int t = 0; t < TW; ++t)
-                        a[t] = fr[(j / 2) * 4 * WAVE + fbase[t][j & 1]];
+            for (int t = 0; t < TA; ++t)
+                a[t] = fr[(j / 2) * 4 * WAVE + fbase[t][j & 1]];
 #pragma unroll
-                    for (int t = 0; t < TW; ++t)
+            for (int t = 0; t < TA; ++t)
 #pragma unroll
-                        for (int g = 0; g < QW; ++g)
-                            acc[t][g] = mfma_step<1>(a[t], qf[g][s], acc[t][g]);
-                });
-                // two k-steps of fragment reads in flight: the reads of k-steps
-                // 0 and 1, then per k-step its MFMAs and the reads two ahead
-                __builtin_amdgcn_sched_group_barrier(0x100, 2 * TW, 0);
-                static_for<0, KSTG>([&](auto J) {
-                    __builtin_amdgcn_sched_group_barrier(0x008, TW * QW, 0);
-                    if constexpr (decltype(J)::value + 2 < KSTG)
-                        __builtin_amdgcn_sched_group_barrier(0x100, TW, 0);
-                });
-            }
-            ++z;
+                for (int g = 0; g < QW; ++g)
+                    ac[t][g] = mfma_step<1>(a[t], qf[g][s], ac[t][g]);
         });
-        if (!active)
-            continue;
-        // ---- candidates of the block: acc = -|x|^2/2 + <q, x>, distance
-        // |q|^2 - 2*acc; a value passes if acc >= nu of its query
+        // two k-steps of fragment reads in flight: the reads of k-steps 0 and
+        // 1, then per k-step its MFMAs and the reads two ahead
+        __builtin_amdgcn_sched_group_barrier(0x100, 2 * TA, 0);
+        static_for<0, KSTG>([&](auto J) {
+            __builtin_amdgcn_sched_group_barrier(0x008, TA * QW, 0);
+            if constexpr (decltype(J)::value + 2 < KSTG)
+                __builtin_amdgcn_sched_group_barrier(0x100, TA, 0);
+        });
+    };
+    // candidates of wave tiles t0 .. t0+TA-1 of block b: acc = -|x|^2/2 +
+    // <q, x>, distance |q|^2 - 2*acc; a value passes if acc >= nu of its query
+    auto test_tiles = [&](f32x4(&ac)[TA][QW], int b, int t0) {
         static_for<0, QW>([&](auto G) {
             constexpr int g = decltype(G)::value;
             float m = -INFINITY;
 #pragma unroll
-            for (int t = 0; t < TW; ++t)
-                m = fmaxf(m, fmaxf(fmaxf(acc[t][g][0], acc[t][g][1]),
-                                   fmaxf(acc[t][g][2], acc[t][g][3])));
+            for (int t = 0; t < TA; ++t)
+                m = fmaxf(m, fmaxf(fmaxf(ac[t][g][0], ac[t][g][1]),
+                                   fmaxf(ac[t][g][2], ac[t][g][3])));
             if (!ballot(m >= nu[g]))
                 return;
             const float qg = qn_w[g * 16 + col];
 #pragma unroll
-            for (int t = 0; t < TW; ++t) {
-                const int tt = RS == 2 ? half : t;
+            for (int t = 0; t < TA; ++t) {
+                const int tt = tile_of(t0 + t);
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    const float a = acc[t][g][e];
+                    const float a = ac[t][g][e];
                     uint64_t mk = ballot(a >= nu[g]);
                     const uint32_t key = f2key(fmaf(-2.f, a, qg));
                     const int32_t idx = (int32_t)(rbeg + b * RQ_ROWS + tt * 16 + jg * 4 + e);
@@ -294,6 +284,131 @@ __global__ __launch_bounds__(RQ_WAVES * WAVE, 1) void rq_scan_kernel(const ScanA
                 }
             }
         });
+    };
+    // this wave's part of stage z has landed once at most FPW*(S-2) loads are
+    // outstanding (the fragment loads of the S-2 stages issued after it); the
+    // barrier then tells that every wave's part has and that every wave is
+    // done with stage z - 1, whose slot the next load reuses
+    auto next_stage = [&](int z) {
+        __builtin_amdgcn_sched_barrier(0);
+        wait_vmcnt<FPW * (S - 2)>();
+        stream_barrier();
+        issue(z + S - 1);
+        __builtin_amdgcn_sched_barrier(0);
+    };
+
+    int z = 0;   // the stage being consumed
+    for (int b = 0; b < n_blk; ++b) {
+        if constexpr (TSEQ) {
+            // one stage per block; its tiles one after the other, each with
+            // its candidate test
+            next_stage(z);
+            const int slot = z % S;
+            if (active) {
+                static_for<0, TW>([&](auto T) {
+                    f32x4 acc[TA][QW];
+                    init_acc(acc, slot, b, T.value);
+                    mfma_tiles(Int<0>{}, acc, slot, T.value);
+                    test_tiles(acc, b, T.value);
+                });
+            }
+            ++z;
+        } else {
+            f32x4 acc[TW][QW];
+            static_for<0, SPB>([&](auto ST) {
+                constexpr int st = decltype(ST)::value;
+                next_stage(z);
+                const int slot = z % S;
+                if constexpr (st == 0) {
+                    // the accumulators start from -|x|^2/2 of their rows (-inf
+                    // for rows past the chunk)
+#pragma unroll
+                    for (int t = 0; t < TW; ++t) {
+                        const int tt = RS == 2 ? half : t;
+                        const f32x4 xn =
+                            *(const f32x4 *)(nslot + slot * WAVE + tt * 16 + jg * 4);
+                        f32x4 h;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            h[e] = b * RQ_ROWS + tt * 16 + jg * 4 + e < nrows ? -0.5f * xn[e]
+                                                                             : -INFINITY;
+#pragma unroll
+                        for (int g = 0; g < QW; ++g)
+                            acc[t][g] = h;
+                    }
+                }
+                if (active) {
+                    // the lane's A fragment of tile tt, k-step j of the stage:
+                    // row col of the tile, quarter jg, at load (j/2)*4 + rg
+                    const i32x4 *fr = ring + slot * F * WAVE;
+                    uint32_t fbase[TW][2];
+#pragma unroll
+                    for (int t = 0; t < TW; ++t) {
+                        const int tt = RS == 2 ? half : t;
+                        const int ri = col & 7, rg = tt * 2 + (col >> 3);
+#pragma unroll
+                        for (int h = 0; h < 2; ++h)
+                            fbase[t][h] = (uint32_t)rg * WAVE + rq_chunk(ri, rg, 4 * h + jg);
+                    }
+                    static_for<0, KSTG>([&](auto J) {
+                        constexpr int j = decltype(J)::value, s = st * KSTG + j;
+                        i32x4 a[TW];
+#pragma unroll
+                        for (int t = 0; t < TW; ++t)
+                            a[t] = fr[(j / 2) * 4 * WAVE + fbase[t][j & 1]];
+#pragma unroll
+                        for (int t = 0; t < TW; ++t)
+#pragma unroll
+                            for (int g = 0; g < QW; ++g)
+                                acc[t][g] = mfma_step<1>(a[t], qf[g][s], acc[t][g]);
+                    });
+                    // two k-steps of fragment reads in flight: the reads of
+                    // k-steps 0 and 1, then per k-step its MFMAs and the
+                    // reads two ahead
+                    __builtin_amdgcn_sched_group_barrier(0x100, 2 * TW, 0);
+                    static_for<0, KSTG>([&](auto J) {
+                        __builtin_amdgcn_sched_group_barrier(0x008, TW * QW, 0);
+                        if constexpr (decltype(J)::value + 2 < KSTG)
+                            __builtin_amdgcn_sched_group_barrier(0x100, TW, 0);
+                    });
+                }
+                ++z;
+            });
+            if (!active)
+                continue;
+            // ---- candidates of the block: acc = -|x|^2/2 + <q, x>, distance
+            // |q|^2 - 2*acc; a value passes if acc >= nu of its query
+            static_for<0, QW>([&](auto G) {
+                constexpr int g = decltype(G)::value;
+                float m = -INFINITY;
+#pragma unroll
+                for (int t = 0; t < TW; ++t)
+                    m = fmaxf(m, fmaxf(fmaxf(acc[t][g][0], acc[t][g][1]),
+                                       fmaxf(acc[t][g][2], acc[t][g][3])));
+                if (!ballot(m >= nu[g]))
+                    return;
+                const float qg = qn_w[g * 16 + col];
+#pragma unroll
+                for (int t = 0; t < TW; ++t) {
+                    const int tt = RS == 2 ? half : t;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const float a = acc[t][g][e];
+                        uint64_t mk = ballot(a >= nu[g]);
+                        const uint32_t key = f2key(fmaf(-2.f, a, qg));
+                        const int32_t idx =
+                            (int32_t)(rbeg + b * RQ_ROWS + tt * 16 + jg * 4 + e);
+                        while (mk) {
+                            const int src = __builtin_ctzll(mk);
+                            mk &= mk - 1;
+                            insert(g, src & 15,
+                                   (uint32_t)__builtin_amdgcn_readlane((int)key, src),
+                                   __builtin_amdgcn_readlane(idx, src));
+                        }
+                    }
+                }
+            });
+        }
     }
 
     // ---- the wave's lists -> workspace [B][n_chunks * RS][k], list c*RS + half
@@ -365,6 +480,7 @@ hipError_t launch_rq_nks(const KnnPlan &p, const ScanArgs &a, hipStream_t s)
         RB_RQ(1, 2)
         RB_RQ(2, 2)
         RB_RQ(4, 2)
+        RB_RQ(4, 1)
     } else if constexpr (NKS == 16 || NKS == 24) {
         RB_RQ(1, 2)
         RB_RQ(2, 2)

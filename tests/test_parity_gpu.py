@@ -109,6 +109,9 @@ KNN_CASES = [
     ("bf16", 40, 30000, 384, 10),   # the same batch over a small bank: the tile scan
     ("bf16", 100, 30000, 384, 20),  # d = 384, (2, 2), k = 20
     ("bf16", 256, 50000, 384, 10),  # d = 384, (4, 2)
+    ("bf16", 512, 60000, 384, 10),  # d = 384, (4, 1): the wide workload's batch, tiles one
+                                    # after the other
+    ("bf16", 300, 20000, 384, 16),  # (4, 1), k = 16: a two-slot ring; a partly filled wave
     ("bf16", 64, 530000, 512, 64),  # d = 512, (1, 2), k = 64
     ("bf16", 128, 40000, 512, 20),  # d = 512, (2, 2)
     ("bf16", 250, 40000, 512, 10),  # d = 512, (2, 1)
