@@ -38,6 +38,7 @@ FP32_PEAK_TFLOPS = 157.3
 # Sources the scan kernel is built from: measured traffic is reported only for
 # the build whose sources it was taken with.
 SCAN_SOURCES = ["paper_2606_17949_amd/csrc/scan.hpp", "paper_2606_17949_amd/csrc/scan_rq.hpp",
+                "paper_2606_17949_amd/csrc/scan_gemm.hpp",
                 "paper_2606_17949_amd/csrc/knn_common.hpp",
                 "paper_2606_17949_amd/csrc/kernels.hpp", "paper_2606_17949_amd/csrc/common.hpp"]
 TRAFFIC_FILE = "profiles/scan_traffic.json"

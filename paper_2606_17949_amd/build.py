@@ -18,7 +18,7 @@ CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "librouteb.so")
 SOURCES = ["api.hip", "knn.hip", "route.hip", "scan_bf16.hip", "scan_bf16_ragged.hip",
            "scan_f32.hip", "scan_f32_ragged.hip", "scan_rq.hip", "scan_rq12.hip", "scan_rq16.hip",
-           "scan_rq24.hip", "scan_rq32.hip"]
+           "scan_rq24.hip", "scan_rq32.hip", "scan_gemm.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

@@ -40,9 +40,21 @@ constexpr int SEED_MAX_GROUPS = 2048;  // S / 16 for S <= 32768
 constexpr int RQ_WAVES = 8;
 constexpr int RQ_ROWS = 32;
 constexpr int RQ_SMALL_B_MIN_ROWS = 2048;   // bank rows per compute unit, batches of <= 64
+// The GEMM-structured scan (bf16 rows, d a multiple of GM_KST, more than 256
+// requests): GM_WAVES waves per workgroup, macro tiles of GM_ROWS bank rows by
+// a tile of GM_QRY requests, K in stages of GM_KST elements in GM_SLOTS LDS
+// slots.
+constexpr int GM_WAVES = 8;
+constexpr int GM_ROWS = 256;
+constexpr int GM_QRY = 256;
+constexpr int GM_KST = 64;
+constexpr int GM_SLOTS = 2;
+constexpr int GM_STAGE = 64;   // per-wave LDS staging of one macro tile's candidates
 
 // How one rb_knn_topk call is split (the tile scan; the query-resident scan
-// differs in that one workgroup holds the whole batch, so n_qt = 1).
+// differs in that one workgroup holds the whole batch, so n_qt = 1; the
+// GEMM-structured scan in its request tiles of GM_QRY, one workgroup per
+// (chunk, tile) with the chunk in macro tiles of GM_ROWS rows).
 //  * seed: S bank rows spread evenly over the bank, scored in groups of 16;
 //    per query, the k-th smallest of 128 of the S/16 group minima (each
 //    lane's two smallest of its share) bounds the k-th nearest distance from
@@ -56,7 +68,7 @@ constexpr int RQ_SMALL_B_MIN_ROWS = 2048;   // bank rows per compute unit, batch
 //  * merge: per query, the k smallest of its W lists (W = n_chunks, times
 //    the row halves rs of the query-resident scan).
 struct KnnPlan {
-    int kind;           // 0 tile scan, 1 query-resident scan
+    int kind;           // 0 tile scan, 1 query-resident scan, 2 GEMM-structured scan
     int qw, rs, spb;    // query-resident scan: query groups per wave, row halves, stages per block,
     int stages;         //   ring slots
     int dtype;          // 0 fp32, 1 bf16

@@ -567,6 +567,17 @@ int plan_knn(int B, int N, int d, int dtype, int k, int num_cu, KnnPlan *p, int 
             }
         }
     }
+    // The GEMM-structured scan takes batches of more than 256 bf16 requests
+    // that the query-resident scan cannot hold, whose rows are a whole
+    // number of its 64-element stages (at least two) and whose lists fit its
+    // LDS beside the stage ring. (With one tile of requests per chunk it
+    // would fetch every bank row from HBM with a single stage of lead, so
+    // smaller batches stay on the other scans.)
+    if (dtype == 1 && B > 256 && p->kind != 1 && d % GM_KST == 0 && d >= 2 * GM_KST &&
+        gemm_layout(k).bytes <= LDS_LIMIT) {
+        p->kind = 2;
+        p->qw = p->rs = p->spb = p->stages = 0;
+    }
     // tile scan: largest query tile that B can fill and whose lists fit in
     // LDS; then as many of its query groups resident in LDS as the rest of
     // the space holds
@@ -603,6 +614,9 @@ int plan_knn(int B, int N, int d, int dtype, int k, int num_cu, KnnPlan *p, int 
     if (p->kind == 1) {
         p->n_qt = 1;
         p->lds_bytes = rq_layout(k, p->qw, p->nks / p->spb, p->stages).bytes;
+    } else if (p->kind == 2) {
+        p->n_qt = (B + GM_QRY - 1) / GM_QRY;
+        p->lds_bytes = gemm_layout(k).bytes;
     }
     // one workgroup per compute unit (the LDS use allows no more); with
     // `reserve`, that many units of each XCD stay free: workgroups go to the
@@ -662,11 +676,16 @@ int plan_knn(int B, int N, int d, int dtype, int k, int num_cu, KnnPlan *p, int 
     off += align256((size_t)B * p->W * k * 4);
     // candidate overflow: per scan wave, every (row, query) pair of one
     // iteration beyond the LDS staging area
+    // (the GEMM-structured scan: per wave, its 64 x 128 values of a macro
+    // tile beyond its LDS staging area)
     const long pairs = (long)SCAN_RT * 16 * p->ng * 16;
-    p->ovf_cap = p->kind == 0 && pairs > STAGE_CAP ? (int)(pairs - STAGE_CAP) : 0;
+    p->ovf_cap = p->kind == 0 && pairs > STAGE_CAP ? (int)(pairs - STAGE_CAP)
+                 : p->kind == 2                    ? 64 * 128 - GM_STAGE
+                                                   : 0;
     p->grid = p->kind == 1 ? p->n_chunks : ((p->n_chunks + 7) / 8) * 8 * p->n_qt;
+    const int waves_per_wg = p->kind == 2 ? GM_WAVES : SCAN_WAVES;
     p->off_ovf = off;
-    off += align256((size_t)p->grid * SCAN_WAVES * 3 * (p->ovf_cap > 0 ? p->ovf_cap : 1) * 4);
+    off += align256((size_t)p->grid * waves_per_wg * 3 * (p->ovf_cap > 0 ? p->ovf_cap : 1) * 4);
     p->bytes = off;
     return 0;
 }
@@ -762,7 +781,9 @@ hipError_t launch_knn(const KnnPlan &p, const void *queries, const void *bank,
         if (timed && (e = hipEventRecord(t_scan_begin, s)) != hipSuccess)
             return e;
         const bool ragged = p.d % (p.dtype == 1 ? 32 : 16) != 0;
-        if (p.kind == 1)
+        if (p.kind == 2)
+            e = launch_scan_gemm(p, a, s);
+        else if (p.kind == 1)
             e = launch_scan_rq(p, a, s);
         else
             e = p.dtype == 1

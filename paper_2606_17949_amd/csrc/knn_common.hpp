@@ -81,9 +81,43 @@ __host__ __device__ inline RqLayout rq_layout(int k, int qw, int kstg, int stage
     return L;
 }
 
+// Byte offsets of the GEMM-structured scan's LDS regions.
+struct GemmLayout {
+    uint32_t ring, norms, list, qn, gb, lmk, nu, sq, sk, si, bytes;
+};
+
+__host__ __device__ inline GemmLayout gemm_layout(int k)
+{
+    GemmLayout L;
+    uint32_t o = 0;
+    L.ring = o;    // [GM_SLOTS][2 * GM_ROWS / 8][64] row and request fragments of a stage
+    o += (uint32_t)GM_SLOTS * (2 * GM_ROWS / 8) * WAVE * 16;
+    L.norms = o;   // [2][GM_ROWS] |x|^2 of a macro tile's rows
+    o += 2u * GM_ROWS * 4;
+    L.list = o;    // [GM_QRY][k] (key << 32 | index), the workgroup's candidate lists
+    o += (uint32_t)GM_QRY * k * 8;
+    L.qn = o;      // [GM_QRY] |q|^2
+    o += GM_QRY * 4;
+    L.gb = o;      // [GM_QRY] snapshot of the shared bound
+    o += GM_QRY * 4;
+    L.lmk = o;     // [GM_QRY] an upper bound of each list's largest key
+    o += GM_QRY * 4;
+    L.nu = o;      // [GM_QRY] each request's candidate threshold on the accumulators
+    o += GM_QRY * 4;
+    L.sq = o;      // [waves][GM_STAGE] staged candidates: tile request,
+    o += GM_WAVES * GM_STAGE * 4;
+    L.sk = o;      //   distance key,
+    o += GM_WAVES * GM_STAGE * 4;
+    L.si = o;      //   bank row
+    o += GM_WAVES * GM_STAGE * 4;
+    L.bytes = o;
+    return L;
+}
+
 // The bank-scan launchers, one translation unit per element type and
 // k-step raggedness (they are the bulk of the compile time), and one per row
 // length for the query-resident scan.
+hipError_t launch_scan_gemm(const KnnPlan &p, const ScanArgs &a, hipStream_t s);
 hipError_t launch_scan_rq(const KnnPlan &p, const ScanArgs &a, hipStream_t s);
 hipError_t launch_scan_rq12(const KnnPlan &p, const ScanArgs &a, hipStream_t s);
 hipError_t launch_scan_rq16(const KnnPlan &p, const ScanArgs &a, hipStream_t s);
@@ -184,6 +218,9 @@ __device__ __forceinline__ void wait_vmcnt()
 template <int I> struct Int {
     static constexpr int value = I;
 };
+template <bool V> struct Bool {
+    static constexpr bool value = V;
+};
 
 // f(Int<I>) for I = B..E-1, unrolled at compile time.
 template <int B, int E, typename F>
@@ -227,6 +264,18 @@ __device__ __forceinline__ void lds_store_relaxed(uint32_t *p, uint32_t v)
 __device__ __forceinline__ uint64_t pack(uint32_t key, int32_t idx)
 {
     return ((uint64_t)key << 32) | (uint32_t)idx;
+}
+
+// 64-bit compare-and-swap in LDS; true when *p held `expect` and now holds `v`.
+__device__ __forceinline__ bool lds_cas64(uint64_t *p, uint64_t expect, uint64_t v)
+{
+    return atomicCAS((unsigned long long *)p, (unsigned long long)expect,
+                     (unsigned long long)v) == (unsigned long long)expect;
+}
+
+__device__ __forceinline__ uint64_t lds_load64(const uint64_t *p)
+{
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
 // Inclusive prefix sum over the wave.

@@ -8,18 +8,6 @@ namespace rb {
 
 namespace {
 
-// 64-bit compare-and-swap in LDS; true when *p held `expect` and now holds `v`.
-__device__ __forceinline__ bool lds_cas64(uint64_t *p, uint64_t expect, uint64_t v)
-{
-    return atomicCAS((unsigned long long *)p, (unsigned long long)expect,
-                     (unsigned long long)v) == (unsigned long long)expect;
-}
-
-__device__ __forceinline__ uint64_t lds_load64(const uint64_t *p)
-{
-    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-}
-
 // One workgroup per (bank chunk, tile of 16*NG queries); SCAN_WAVES waves, two
 // per SIMD. Each wave owns 16*RT consecutive rows of every
 // SCAN_WAVES*16*RT-row iteration and holds their inner products with all tile

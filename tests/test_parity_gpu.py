@@ -118,6 +118,14 @@ KNN_CASES = [
     ("bf16", 64, 530000, 1024, 10), # d = 1024, (1, 2)
     ("bf16", 128, 30000, 1024, 64), # d = 1024, (1, 1), k = 64: half-block stages
     ("bf16", 100, 40, 1024, 33),    # fewer rows than chunks
+    # more than 256 bf16 requests whose rows are whole 64-element lines, k <= 10,
+    # take the GEMM-structured scan: 256 x 256 macro tiles, 32x32x16 MFMAs
+    ("bf16", 257, 3000, 128, 10),   # a second request tile of one request; two stages per tile
+    ("bf16", 600, 20000, 384, 10),  # three request tiles, the last partly filled
+    ("bf16", 1024, 50000, 1024, 10),# four request tiles: the largebatch shape over a small bank
+    ("bf16", 513, 10007, 768, 5),   # ragged bank: the last macro tile of a chunk partly filled
+    ("bf16", 400, 30, 256, 10),     # fewer rows than one macro tile, most chunks empty
+    ("bf16", 300, 100000, 512, 1),  # k = 1
 ]
 
 
@@ -145,6 +153,7 @@ def test_knn_exact_ties_take_lower_index():
     ("query-resident scan", 200, 70000, 768, 10),
     ("seeded tile scan, one tile", 64, 70000, 768, 10),
     ("seeded tile scan, two tiles", 300, 66000, 256, 16),
+    ("GEMM-structured scan", 300, 66000, 256, 10),
 ])
 def test_knn_exact_ties_across_kth(label, B, N, d, k):
     """Duplicated rows straddling the k-th position: each request's k-th

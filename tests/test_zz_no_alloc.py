@@ -76,7 +76,9 @@ def test_noalloc_matches_route_batch():
 
 def test_noalloc_refuses_sizes_past_its_workspace():
     import paper_2606_17949_amd as rb
-    cfg = synth.tiny_config(B=512, N=100_000, d=384, dtype="bf16", clusters=256)
+    # (a batch of 1024 requests of 384 elements goes to the GEMM-structured
+    # scan, whose per-wave overflow areas alone exceed the static workspace)
+    cfg = synth.tiny_config(B=1024, N=100_000, d=384, dtype="bf16", clusters=256)
     need = rb.rb_workspace_size(cfg.B, cfg.N, cfg.d, rb.RB_BF16, cfg.k, cfg.M)
     say(f"noalloc refusal: B={cfg.B} needs {need / 2**20:.1f} MiB of {rb.RB_SCRATCH_BYTES >> 20}")
     assert need > rb.RB_SCRATCH_BYTES
