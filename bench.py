@@ -60,17 +60,23 @@ def scan_source_digest():
     return h.hexdigest()
 
 
+def _load_traffic(path):
+    """The per-workload traffic records of a scan_traffic.json ({} if none)."""
+    try:
+        with open(path) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return {}
+    return t.get("workloads", {}) if isinstance(t, dict) else {}
+
+
 def measured_traffic(workload):
     """HBM bytes per scan launch from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE
     passes (scaled by the copy calibration), or None when they were taken on other
-    sources or another workload."""
+    sources or not for this workload."""
     root = os.path.dirname(os.path.abspath(__file__))
-    try:
-        with open(os.path.join(root, TRAFFIC_FILE)) as f:
-            t = json.load(f)
-    except (OSError, ValueError):
-        return None
-    if t.get("sources_sha256") != scan_source_digest() or t.get("workload") != workload:
+    t = _load_traffic(os.path.join(root, TRAFFIC_FILE)).get(workload)
+    if not t or t.get("sources_sha256") != scan_source_digest():
         return None
     return t.get("bytes_per_launch")
 
@@ -95,9 +101,10 @@ def parse():
     ap.add_argument("--cpu-sample", type=int, default=0,
                     help="requests in the CPU oracle sample (0: 8 per host thread)")
     ap.add_argument("--record-traffic", metavar="PMC_DIR",
-                    help="turn rocprofv3 FETCH_SIZE/WRITE_SIZE passes over the scan (PMC_DIR/fetch, "
-                         "PMC_DIR/write) and over --calibrate-copy (PMC_DIR/copyfetch, "
-                         "PMC_DIR/copywrite) into PMC_DIR/scan_traffic.json for --workload")
+                    help="turn rocprofv3 FETCH_SIZE/WRITE_SIZE passes over the scan "
+                         "(PMC_DIR/<workload>/fetch, PMC_DIR/<workload>/write) and over "
+                         "--calibrate-copy (PMC_DIR/copyfetch, PMC_DIR/copywrite) into the "
+                         "--workload record of PMC_DIR/scan_traffic.json")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain device copy of 1 GiB (counter calibration)")
     ap.add_argument("--ceilings", action="store_true",
@@ -173,21 +180,29 @@ def _counter_means(path, kernel_sub, counter):
 
 def record_traffic(pmc, workload):
     """Scan HBM bytes per launch: counter KiB x (bytes a 1 GiB copy moves / the
-    same counter's KiB for that copy)."""
+    same counter's KiB for that copy). Reads PMC/copyfetch, PMC/copywrite and
+    PMC/<workload>/fetch, PMC/<workload>/write; writes PMC/scan_traffic.json,
+    the records already there (else the committed ones) with this workload's
+    replaced."""
     copy_bytes = float(1 << 30)
     cf, _ = _counter_means(os.path.join(pmc, "copyfetch"), "copyBuffer", "FETCH_SIZE")
     cw, _ = _counter_means(os.path.join(pmc, "copywrite"), "copyBuffer", "WRITE_SIZE")
-    sf, nf = _counter_means(os.path.join(pmc, "fetch"), "scan_kernel", "FETCH_SIZE")
-    sw, nw = _counter_means(os.path.join(pmc, "write"), "scan_kernel", "WRITE_SIZE")
+    sf, nf = _counter_means(os.path.join(pmc, workload, "fetch"), "scan_kernel", "FETCH_SIZE")
+    sw, nw = _counter_means(os.path.join(pmc, workload, "write"), "scan_kernel", "WRITE_SIZE")
     kf, kw = copy_bytes / cf, copy_bytes / cw     # bytes per counter unit
-    out = {"workload": workload, "sources_sha256": scan_source_digest(),
+    rec = {"sources_sha256": scan_source_digest(),
            "fetch_size_kib": round(sf, 1), "write_size_kib": round(sw, 1), "dispatches": [nf, nw],
            "copy_fetch_kib_per_gib": round(cf, 1), "copy_write_kib_per_gib": round(cw, 1),
            "fetch_bytes": round(sf * kf), "write_bytes": round(sw * kw),
            "bytes_per_launch": round(sf * kf + sw * kw)}
-    with open(os.path.join(pmc, "scan_traffic.json"), "w") as f:
-        json.dump(out, f, indent=1)
-    print(json.dumps(out), flush=True)
+    out_path = os.path.join(pmc, "scan_traffic.json")
+    recs = _load_traffic(out_path)
+    if not recs:
+        recs = _load_traffic(os.path.join(os.path.dirname(os.path.abspath(__file__)), TRAFFIC_FILE))
+    recs[workload] = rec
+    with open(out_path, "w") as f:
+        json.dump({"workloads": recs}, f, indent=1, sort_keys=True)
+    print(json.dumps({workload: rec}), flush=True)
 
 
 def main():

@@ -22,13 +22,21 @@ __device__ __forceinline__ void dma4(__amdgpu_buffer_rsrc_t r, float *dst, uint3
 // eight 16-byte chunks of one line per group of 8 lanes), so every line is
 // fetched by one instruction. In LDS, load f of a stage (row group
 // rg = f % 4 of the block, k-step pair f / 4) holds row rg*8 + ri's chunk c
-// (quarter c % 4 of k-step 2*(f/4) + c/4) at position 8*ri + (c ^ ri ^ (rg & 1)).
-// The XOR spreads the 16 rows of a tile over distinct LDS bank groups, so
-// the MFMA A-fragment read (lane (col, jg): row col, quarter jg of one
-// k-step) is conflict free.
+// (quarter c % 4 of k-step 2*(f/4) + c/4) at position
+// 8*ri + (c ^ rq_perm(ri) ^ 2*(rg & 1)), rq_perm taking the row pairs of a
+// group to 0, 1, 4, 5. The MFMA A-fragment read (lane (col, jg): row col,
+// quarter jg of one k-step) then puts the sixteen lanes that LDS serves
+// together (lanes 8p..8p+7 and 32+8p..32+8p+7: eight rows at quarters jg
+// and jg + 2) on distinct bank groups, as it does the sixteen rows of one
+// quarter: no bank conflicts (a plain XOR with the row, which spreads only
+// the latter, costs four conflict cycles per read).
+__device__ __forceinline__ int rq_perm(int ri)
+{
+    return ((ri >> 1) & 1) | ((ri >> 2) << 2);
+}
 __device__ __forceinline__ uint32_t rq_chunk(int ri, int rg, int c)
 {
-    return (uint32_t)(8 * ri + (c ^ ri ^ (rg & 1)));
+    return (uint32_t)(8 * ri + (c ^ rq_perm(ri) ^ (2 * (rg & 1))));
 }
 
 // One workgroup per bank chunk; RQ_WAVES waves, two per SIMD, in RS row
@@ -146,7 +154,7 @@ __global__ __launch_bounds__(RQ_WAVES * WAVE, 1) void rq_scan_kernel(const ScanA
     // this lane's place in a load: row ri of the row group, the chunk of the
     // 128-byte line that lands at its position (rq_chunk inverted)
     const int dri = lane >> 3;
-    auto dma_chunk = [&](int rg) { return (lane & 7) ^ dri ^ (rg & 1); };
+    auto dma_chunk = [&](int rg) { return (lane & 7) ^ rq_perm(dri) ^ (2 * (rg & 1)); };
     auto issue = [&](int z) {
         const int slot = z % S, bz = z / SPB, st = z - bz * SPB;
         const bool real = z < n_stg;
