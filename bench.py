@@ -110,6 +110,10 @@ def parse():
     ap.add_argument("--ceilings", action="store_true",
                     help="only measure the practical ceilings: a read-only pass over 4 GiB and "
                          "a library bf16 GEMM of the largebatch shape (yardsticks, not the path)")
+    ap.add_argument("--graph", action="store_true",
+                    help="sequential batches, each batch's calls (rb_route_batch, "
+                         "rb_advance_state) captured beforehand in a HIP graph of its own; "
+                         "times the graph launches (the host-side cost of small batches)")
     ap.add_argument("--cold", action="store_true",
                     help="time each batch alone (sequential) right after reading a 512 MiB "
                          "buffer on the same stream, so that the bank is not resident in the "
@@ -399,6 +403,37 @@ def main():
               flush=True)
         return
 
+    if args.graph:
+        if args.schedule != "sequential" or opts is not None:
+            raise SystemExit("--graph captures the sequential schedule without --options")
+        # the timed batches' calls, one graph per batch (kernel nodes only:
+        # the library enqueues no memset or copy)
+        cap = torch.cuda.Stream(device=dev)
+        graphs = {}
+        torch.cuda.synchronize()
+        for t in range(W, W + K):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=cap, capture_error_mode="thread_local"):
+                rb.rb_route_batch(queries[t], bank, norms, cfg.k, g_qual, g_len, plens[t], inst,
+                                  cfg.weights, ws=ws, assign=assign[t], stream=cap)
+                rb.rb_advance_state(inst, carry_dt, stream=cap)
+            graphs[t] = g
+        torch.cuda.synchronize()
+        b0, b1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        b0.record(stream)
+        w0 = time.perf_counter()
+        for t in range(W, W + K):
+            graphs[t].replay()
+        b1.record(stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - w0
+        ms = b0.elapsed_time(b1) / K
+        print(json.dumps({"metric": "routing decisions/sec, sequential batches as HIP graphs",
+                          "value": round(cfg.B / (ms / 1e3), 1), "unit": "decisions/s",
+                          "workload": cfg.name, "batches": K, "ms_per_batch": round(ms, 4),
+                          "host_us_per_batch": round(wall / K * 1e6, 1)}), flush=True)
+        return
+
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -476,32 +511,57 @@ def main():
     print(json.dumps(out), flush=True)
 
 
+def cpu_model():
+    """The host CPU's model name (Linux /proc/cpuinfo), or None."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def cpu_baseline(cfg, bank, queries, qual, length, plen, inst_h, sample, opt_names=(),
                  budget=None, mask=None):
     """The oracle as it stands on a bounded sample: the first S requests of the
     first timed batch, full k-NN over the whole bank, predictions and the greedy
     assignment (with the same options), on all host threads available to this
-    process."""
+    process; for the two small workloads also on one thread."""
     import numpy as np
 
     import oracle
     threads = len(os.sched_getaffinity(0))
-    S = sample if sample > 0 else min(cfg.B, 16 * threads)
+    S = min(cfg.B, sample if sample > 0 else 16 * threads)
     log(f"cpu baseline: oracle on {S} requests, {threads} threads ...")
     bank_h = bank.cpu()
     q_h = queries[:S].cpu()
-    t0 = time.perf_counter()
-    idx, dist = oracle.knn(q_h, bank_h, cfg.k, nthreads=threads)
-    qh, lh = oracle.predict(idx, qual, length, dist=dist,
-                            weighting="inv_dist" if "inv_dist" in opt_names else "uniform")
-    oracle.assign(qh, lh, plen[:S], inst_h, cfg.weights,
-                  order="lpt" if "lpt" in opt_names else "arrival",
-                  budget=None if budget is None else budget[:S], mask=mask)
-    dt = time.perf_counter() - t0
+
+    def run(nthreads):
+        t0 = time.perf_counter()
+        idx, dist = oracle.knn(q_h, bank_h, cfg.k, nthreads=nthreads)
+        qh, lh = oracle.predict(idx, qual, length, dist=dist,
+                                weighting="inv_dist" if "inv_dist" in opt_names else "uniform")
+        oracle.assign(qh, lh, plen[:S], inst_h, cfg.weights,
+                      order="lpt" if "lpt" in opt_names else "arrival",
+                      budget=None if budget is None else budget[:S], mask=mask)
+        return time.perf_counter() - t0
+
+    dt = run(threads)
     log(f"cpu baseline: {dt:.1f}s")
-    return {"value": round(S / dt, 3), "unit": "decisions/s", "cores": threads, "kind": "oracle",
-            "sample": f"first {S} requests of one {cfg.B}-request batch: exact fp64 k-NN over "
-                      f"all {cfg.N} bank rows, predictions, greedy assignment ({dt:.1f} s)"}
+    out = {"value": round(S / dt, 3), "unit": "decisions/s", "cores": threads, "kind": "oracle",
+           "sample": f"first {S} requests of one {cfg.B}-request batch: exact fp64 k-NN over "
+                     f"all {cfg.N} bank rows, predictions, greedy assignment ({dt:.1f} s)",
+           "cpu_model": cpu_model()}
+    if S == cfg.B:
+        out["s_per_batch"] = round(dt, 3)
+    if cfg.name in ("tiny", "online"):
+        d1 = run(1)
+        log(f"cpu baseline, one thread: {d1:.1f}s")
+        out["single_thread"] = {"value": round(S / d1, 3), "unit": "decisions/s",
+                                "s_for_sample": round(d1, 3)}
+    return out
 
 
 if __name__ == "__main__":
