@@ -110,6 +110,11 @@ def parse():
     ap.add_argument("--ceilings", action="store_true",
                     help="only measure the practical ceilings: a read-only pass over 4 GiB and "
                          "a library bf16 GEMM of the largebatch shape (yardsticks, not the path)")
+    ap.add_argument("--clock-warm", type=float, default=1.0, metavar="SECONDS",
+                    help="untimed lookups of the first batch (k-NN and label average only, the "
+                         "instance state untouched) for this long before the warm-up batches, "
+                         "so that the timed batches run at the GPU's sustained clock, as in a "
+                         "serving loop that never idles (0: none)")
     ap.add_argument("--graph", action="store_true",
                     help="sequential batches, each batch's calls (rb_route_batch, "
                          "rb_advance_state) captured beforehand in a HIP graph of its own; "
@@ -355,6 +360,29 @@ def main():
                 decide(t)
         rb.rb_profile_scan_events(None, None)
 
+    if args.clock_warm > 0:
+        # the GPU raises its clock only under sustained load (measured in the
+        # scan kernel with s_memtime against the 100 MHz counter: about
+        # 1.65-1.85 GHz after a few batches, 1.93-2.12 GHz after a few hundred)
+        qh_w = torch.empty(cfg.B, cfg.M, device=dev)
+        lh_w = torch.empty(cfg.B, cfg.M, device=dev)
+
+        def warm(n):
+            for _ in range(n):
+                rb.rb_knn_predict(queries[0], bank, norms, cfg.k, g_qual, g_len, ws=ws, q_hat=qh_w,
+                                  l_hat=lh_w, stream=stream)
+        warm(2)
+        torch.cuda.synchronize()
+        t_w = time.perf_counter()
+        warm(8)
+        torch.cuda.synchronize()
+        per = (time.perf_counter() - t_w) / 8
+        # one unbroken stretch of load (no host synchronisation inside it)
+        n_w = max(1, int(args.clock_warm / per))
+        t_w = time.perf_counter()
+        warm(n_w)
+        torch.cuda.synchronize()
+        log(f"clock warm-up: {n_w} untimed lookups in {time.perf_counter() - t_w:.2f} s")
     run(list(range(W)))
     torch.cuda.synchronize()
     log("warm-up done")

@@ -344,7 +344,7 @@ __global__ __launch_bounds__(GM_WAVES * WAVE, 1) void gemm_scan_kernel(const Sca
         kc = 0;
         // ---- end of macro tile rt: acc = <q, x>; v = acc - |x|^2/2 (-inf for
         // rows past the chunk), distance |q|^2 - 2*v. Phase 1: stage every
-        // candidate (v >= nu of its request), in (request tile, row tile,
+        // candidate (v >= nu of its request), in (row tile, request tile,
         // register, lane) order.
         const float *nm = nslot + (rt & 1) * GM_ROWS;
         const int rbase = rt * GM_ROWS;
@@ -363,22 +363,26 @@ __global__ __launch_bounds__(GM_WAVES * WAVE, 1) void gemm_scan_kernel(const Sca
 #pragma unroll
         for (int u = 0; u < TPQ; ++u)
             nus[u] = __uint_as_float(lds_load_relaxed(nu_s + 128 * wq + 32 * u + (lane & 31)));
-        // one 32 x 32 tile at a time (the scheduling barriers keep the
-        // compiler from reading every accumulator out at once)
-        static_for<0, TPQ>([&](auto U) {
-            constexpr int u = decltype(U)::value;
-            const int qi = 128 * wq + 32 * u + (lane & 31);
-            static_for<0, TPR>([&](auto I) {
-                constexpr int i = decltype(I)::value;
+        // row tile by row tile (its rows' norms read once for its four
+        // request tiles), one 32 x 32 tile at a time (the scheduling barriers
+        // keep the compiler from reading every accumulator out at once)
+        static_for<0, TPR>([&](auto I) {
+            constexpr int i = decltype(I)::value;
+            f32x4 h[4];
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+                h[g] = half_norms(i, g);
+            static_for<0, TPQ>([&](auto U) {
+                constexpr int u = decltype(U)::value;
+                const int qi = 128 * wq + 32 * u + (lane & 31);
                 __builtin_amdgcn_sched_barrier(0);
                 float v[16];
                 float m = -INFINITY;
 #pragma unroll
                 for (int g = 0; g < 4; ++g) {
-                    const f32x4 h = half_norms(i, g);
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
-                        v[4 * g + e] = acc[i][u][4 * g + e] + h[e];
+                        v[4 * g + e] = acc[i][u][4 * g + e] + h[g][e];
                         m = fmaxf(m, v[4 * g + e]);
                     }
                 }
