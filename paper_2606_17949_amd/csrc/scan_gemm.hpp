@@ -126,8 +126,8 @@ __global__ __launch_bounds__(GM_WAVES * WAVE, 1) void gemm_scan_kernel(const Sca
               lo + (uint32_t)r0 * rowb + (uint32_t)kc * (GM_KST * 2));
     };
     // with a macro tile's first stage, the last wave loads the tile's norms
-    // (into slot rt & 1: they are read after the macro tile's last stage,
-    // when the next tile's norms are already loading)
+    // into slot rt & 1 (they are read when that stage's MFMAs begin, before
+    // the loads of tile rt + 2 reuse the slot)
     auto issue_norms = [&](int z) {
         const int rt = z / nks;
         if (z - rt * nks == 0 && wave == GM_WAVES - 1)
@@ -298,13 +298,25 @@ __global__ __launch_bounds__(GM_WAVES * WAVE, 1) void gemm_scan_kernel(const Sca
     for (int z = 0, rt = 0, kc = 0; z < n_stg; ++z) {
         const uint32_t rs = (uint32_t)(z & 1) << 16, rn = rs ^ (1u << 16);
         if (kc == 0) {
+            // a macro tile's accumulators start from -|x|^2/2 of their rows
+            // (-inf for rows past the chunk), so that they end as
+            // <q, x> - |x|^2/2; the tile's norms landed two barriers ago
+            const float *nm = nslot + (rt & 1) * GM_ROWS;
 #pragma unroll
-            for (int i = 0; i < TPR; ++i)
+            for (int i = 0; i < TPR; ++i) {
 #pragma unroll
-                for (int u = 0; u < TPQ; ++u)
+                for (int g = 0; g < 4; ++g) {
+                    const int r0 = 64 * wr + 32 * i + 8 * g + 4 * hl;
+                    const f32x4 xn = *(const f32x4 *)(nm + r0);
 #pragma unroll
-                    for (int r = 0; r < 16; ++r)
-                        acc[i][u][r] = 0.f;
+                    for (int e = 0; e < 4; ++e) {
+                        const float h = rt * GM_ROWS + r0 + e < nrows ? -0.5f * xn[e] : -INFINITY;
+#pragma unroll
+                        for (int u = 0; u < TPQ; ++u)
+                            acc[i][u][4 * g + e] = h;
+                    }
+                }
+            }
         }
         // k-steps 0-2 of the stage, each with the next one's fragment reads;
         // k-step 0 also sends the second half of the loads of stage z + 1
@@ -342,50 +354,29 @@ __global__ __launch_bounds__(GM_WAVES * WAVE, 1) void gemm_scan_kernel(const Sca
             continue;
         }
         kc = 0;
-        // ---- end of macro tile rt: acc = <q, x>; v = acc - |x|^2/2 (-inf for
-        // rows past the chunk), distance |q|^2 - 2*v. Phase 1: stage every
+        // ---- end of macro tile rt: acc = v = <q, x> - |x|^2/2 (-inf for rows
+        // past the chunk), distance |q|^2 - 2*v. Phase 1: stage every
         // candidate (v >= nu of its request), in (row tile, request tile,
         // register, lane) order.
-        const float *nm = nslot + (rt & 1) * GM_ROWS;
         const int rbase = rt * GM_ROWS;
-        // -|x|^2/2 of the rows of register group g of row tile i
-        auto half_norms = [&](int i, int g) -> f32x4 {
-            const int r0 = 64 * wr + 32 * i + 8 * g + 4 * hl;
-            const f32x4 xn = *(const f32x4 *)(nm + r0);
-            f32x4 h;
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-                h[e] = rbase + r0 + e < nrows ? -0.5f * xn[e] : -INFINITY;
-            return h;
-        };
         int nst = 0;
         float nus[TPQ];
 #pragma unroll
         for (int u = 0; u < TPQ; ++u)
             nus[u] = __uint_as_float(lds_load_relaxed(nu_s + 128 * wq + 32 * u + (lane & 31)));
-        // row tile by row tile (its rows' norms read once for its four
-        // request tiles), one 32 x 32 tile at a time (the scheduling barriers
-        // keep the compiler from reading every accumulator out at once)
+        // one 32 x 32 tile at a time (the scheduling barriers keep the
+        // compiler from reading every accumulator out at once)
         static_for<0, TPR>([&](auto I) {
             constexpr int i = decltype(I)::value;
-            f32x4 h[4];
-#pragma unroll
-            for (int g = 0; g < 4; ++g)
-                h[g] = half_norms(i, g);
             static_for<0, TPQ>([&](auto U) {
                 constexpr int u = decltype(U)::value;
                 const int qi = 128 * wq + 32 * u + (lane & 31);
                 __builtin_amdgcn_sched_barrier(0);
-                float v[16];
-                float m = -INFINITY;
+                const f32x16 &v = acc[i][u];
+                float m = v[0];
 #pragma unroll
-                for (int g = 0; g < 4; ++g) {
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        v[4 * g + e] = acc[i][u][4 * g + e] + h[g][e];
-                        m = fmaxf(m, v[4 * g + e]);
-                    }
-                }
+                for (int r = 1; r < 16; ++r)
+                    m = fmaxf(m, v[r]);
                 if (ballot(m >= nus[u])) {
                     const float qq = qn_s[qi];
 #pragma unroll
