@@ -621,12 +621,18 @@ int plan_knn(int B, int N, int d, int dtype, int k, int num_cu, KnnPlan *p, int 
     // one workgroup per compute unit (the LDS use allows no more); with
     // `reserve`, that many units of each XCD stay free: workgroups go to the
     // XCDs round robin and the tiles of a chunk share its XCD, so a whole
-    // number of chunks per XCD is kept below the XCD's unit count
+    // number of chunks per XCD is kept below the XCD's unit count. The GEMM
+    // scan also fills the units that this leaves over (up to n_qt - 1 per
+    // XCD): its last n_chunks % 8 chunks are spread over neighbouring XCDs,
+    // at most two per chunk for four request tiles (measured at B = 1,024,
+    // d = 1,024: 248 workgroups 1,821 us per launch against 1,942 us for 224)
     long chunks = num_cu / p->n_qt;
     if (reserve > 0) {
         const long per_xcd = (num_cu / 8 - reserve) / p->n_qt;
         if (per_xcd >= 1)
             chunks = per_xcd * 8;
+        if (p->kind == 2)
+            chunks = (num_cu - 8L * reserve) / p->n_qt;
     }
     if (chunks < 1)
         chunks = 1;

@@ -65,11 +65,25 @@ __global__ __launch_bounds__(GM_WAVES * WAVE, 1) void gemm_scan_kernel(const Sca
     uint32_t *nu_s = (uint32_t *)(smem + L.nu);      // [GM_QRY] candidate threshold (float bits)
 
     // Workgroup -> (chunk c, request tile t): workgroups go to the eight
-    // XCDs round robin, so every request tile of one chunk lands on one XCD.
+    // XCDs round robin, so every request tile of one of the first
+    // 8 * (n_chunks / 8) chunks lands on one XCD. The last n_chunks % 8
+    // chunks take the remaining workgroups in order of XCD (x) and then of
+    // dispatch (s): rank L among them, chunk base + L / n_qt, tile L % n_qt,
+    // so that a chunk's tiles sit on as few XCDs as the counts allow.
     const int per8 = 8 * A.n_qt;
-    const int rem = blockIdx.x % per8;
-    const int t = rem / 8;
-    const int c = (blockIdx.x / per8) * 8 + rem % 8;
+    const int full = (A.n_chunks / 8) * per8;
+    int t, c;
+    if ((int)blockIdx.x < full) {
+        const int rem = blockIdx.x % per8;
+        t = rem / 8;
+        c = (blockIdx.x / per8) * 8 + rem % 8;
+    } else {
+        const int j = blockIdx.x - full, x = j % 8, s = j / 8;
+        const int tail = (A.n_chunks % 8) * A.n_qt, q = tail / 8, r = tail % 8;
+        const int L = x * q + min(x, r) + s;
+        t = L % A.n_qt;
+        c = s < q + (x < r) ? (A.n_chunks / 8) * 8 + L / A.n_qt : A.n_chunks;
+    }
     if (c >= A.n_chunks)
         return;
     const int tid = threadIdx.x, lane = tid & 63;
