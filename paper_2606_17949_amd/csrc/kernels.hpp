@@ -40,6 +40,7 @@ constexpr int SEED_MAX_GROUPS = 2048;  // S / 16 for S <= 32768
 constexpr int RQ_WAVES = 8;
 constexpr int RQ_ROWS = 32;
 constexpr int RQ_SMALL_B_MIN_ROWS = 2048;   // bank rows per compute unit, batches of <= 64
+constexpr int RQ_SPLIT_MIN_ROWS = 1024;     // chunk rows from which the scan may go in two passes
 // The GEMM-structured scan (bf16 rows, d a multiple of GM_KST, more than 256
 // requests): GM_WAVES waves per workgroup, macro tiles of GM_ROWS bank rows by
 // a tile of GM_QRY requests, K in stages of GM_KST elements in GM_SLOTS LDS
@@ -75,9 +76,10 @@ struct KnnPlan {
     int B, N, d, k;
     int nks, nksp;      // 64-byte k-steps per row, padded to SCAN_KPAD
     int ng, gr, rt;     // query groups of 16 per tile (gr of them resident), 16-row tiles per wave
-    int n_qt, n_chunks, W;
+    int n_qt, n_chunks, W;   // request tiles, bank chunks, lists per query the scan leaves
     long rows_per_chunk;
     int S, G;           // seed rows and groups (0 = no seed)
+    int rq_split;       // query-resident scan: rows of every chunk in its first pass (0 = one pass)
     int grid;           // scan workgroups
     int ovf_cap;        // candidates per scan wave that the workspace takes past LDS
     size_t lds_bytes;

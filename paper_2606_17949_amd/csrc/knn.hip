@@ -237,6 +237,71 @@ __global__ __launch_bounds__(WAVE) void seed_bound_kernel(const uint8_t *__restr
     }
 }
 
+// ------------------------------------------------------------------ list bound
+
+// The shared bound after a first pass over part of every chunk: per query,
+// the k-th smallest key among the entries of its first nl lists (of W),
+// when there are at least k. Any k of the entries are distances of k
+// distinct bank rows, so each lane keeps only its LB_KEEP smallest, and the
+// k-th smallest of those kept, an upper bound of the k-th nearest distance
+// (the exact k-th smallest unless more than LB_KEEP of the k smallest are one
+// lane's), lowers the bound. One wave per query: k rounds each take the
+// wave's smallest kept key out of its lane.
+constexpr int LB_KEEP = 16;
+__global__ __launch_bounds__(WAVE) void list_bound_kernel(const int32_t *__restrict__ ccnt,
+                                                         const uint32_t *__restrict__ ckey,
+                                                         int W, int nl, int k,
+                                                         uint32_t *__restrict__ tau)
+{
+    const int b = blockIdx.x, lane = lane_id();
+    const int32_t *cnt = ccnt + (size_t)b * W;
+    const uint32_t *key = ckey + (size_t)b * W * k;
+    uint32_t v[LB_KEEP];   // ascending; KEY_NONE: empty
+#pragma unroll
+    for (int i = 0; i < LB_KEEP; ++i)
+        v[i] = KEY_NONE;
+    // four lists per lane at a time: their lengths, then their entries
+    for (int w0 = 0; w0 < nl; w0 += 4 * WAVE) {
+        int m[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int w = w0 + u * WAVE + lane;
+            m[u] = w < nl ? cnt[w] : 0;
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const uint32_t *kw = key + (size_t)(w0 + u * WAVE + lane) * k;
+            for (int j = 0; j < m[u]; ++j) {
+                uint32_t x = kw[j];
+#pragma unroll
+                for (int i = 0; i < LB_KEEP; ++i) {
+                    const uint32_t lo = min(v[i], x);
+                    x = max(v[i], x);
+                    v[i] = lo;
+                }
+            }
+        }
+    }
+    uint32_t kth = KEY_NONE;
+    for (int r = 0; r < k; ++r) {
+        uint32_t mn = v[0];
+#pragma unroll
+        for (int o = 1; o < WAVE; o <<= 1)
+            mn = min(mn, (uint32_t)__shfl_xor((int)mn, o));
+        if (mn == KEY_NONE)
+            return;   // fewer than k keys (keys are below KEY_NONE)
+        if (lane == __builtin_ctzll(ballot(v[0] == mn))) {
+#pragma unroll
+            for (int i = 0; i + 1 < LB_KEEP; ++i)
+                v[i] = v[i + 1];
+            v[LB_KEEP - 1] = KEY_NONE;
+        }
+        kth = mn;
+    }
+    if (lane == 0 && kth < tau[b])
+        tau[b] = kth;
+}
+
 // ------------------------------------------------------------------ merge
 
 struct MergeArgs {
@@ -651,9 +716,6 @@ int plan_knn(int B, int N, int d, int dtype, int k, int num_cu, KnnPlan *p, int 
     }
     p->rows_per_chunk = rpc;
     p->n_chunks = (int)(((long)N + rpc - 1) / rpc);
-    p->W = p->n_chunks * (p->kind == 1 ? p->rs : 1);
-    if (p->W > MERGE_MAX_LISTS)
-        return -1;
     // seed sample: about N/32 rows, 2048..32768, a multiple of 64 and at most N
     long S = N / 32;
     if (S < 2048)
@@ -667,6 +729,24 @@ int plan_knn(int B, int N, int d, int dtype, int k, int num_cu, KnnPlan *p, int 
         S = 0;
     p->S = (int)S;
     p->G = (int)(S / 16);
+    // The query-resident scan goes in two passes when the seed covers less
+    // than 1/32 of a long bank (N / 32 above the largest seed, 32,768 rows)
+    // and the batch exceeds 128 requests: the first pass takes the first eighth of every chunk, the
+    // k-th smallest entry of its lists then bounds the second, over the rest,
+    // which leaves a second set of lists. The bank is still read once and the
+    // second pass runs under the bound of a sample of an eighth of the bank.
+    // (Measured, one pass against two: B = 512, N = 4,000,000, d = 384
+    // 1,656 against 1,497 us; B = 256, N = 1,000,000, d = 768, where the seed
+    // already covers N/32, 446-450 against 437-444; B <= 128 10-13 % slower
+    // in two passes: the second launch's start outweighs the fewer
+    // candidates.)
+    p->rq_split = 0;
+    if (p->kind == 1 && B > 128 && (long)N / 32 > 16L * SEED_MAX_GROUPS &&
+        p->rows_per_chunk >= RQ_SPLIT_MIN_ROWS)
+        p->rq_split = (int)(p->rows_per_chunk / 8 / RQ_ROWS * RQ_ROWS);
+    p->W = p->n_chunks * (p->kind == 1 ? p->rs : 1) * (p->rq_split > 0 ? 2 : 1);
+    if (p->W > MERGE_MAX_LISTS)
+        return -1;
     size_t off = 0;
     p->off_tau = off;
     off += align256((size_t)B * 4);
@@ -777,6 +857,10 @@ hipError_t launch_knn(const KnnPlan &p, const void *queries, const void *bank,
         a.n_chunks = p.n_chunks;
         a.n_qt = p.n_qt;
         a.rows_per_chunk = p.rows_per_chunk;
+        a.row_lo = 0;
+        a.row_hi = p.rows_per_chunk;
+        a.n_lists = p.W;
+        a.list_base = 0;
         a.tau = tau;
         a.ccnt = ccnt;
         a.ckey = ckey;
@@ -789,7 +873,20 @@ hipError_t launch_knn(const KnnPlan &p, const void *queries, const void *bank,
         const bool ragged = p.d % (p.dtype == 1 ? 32 : 16) != 0;
         if (p.kind == 2)
             e = launch_scan_gemm(p, a, s);
-        else if (p.kind == 1)
+        else if (p.kind == 1 && p.rq_split > 0) {
+            a.row_hi = p.rq_split;
+            e = launch_scan_rq(p, a, s);
+            if (e == hipSuccess) {
+                hipLaunchKernelGGL(list_bound_kernel, dim3(p.B), dim3(WAVE), 0, s, ccnt, ckey,
+                                   p.W, p.W / 2, p.k, tau);
+                e = hipGetLastError();
+            }
+            a.row_lo = p.rq_split;
+            a.row_hi = p.rows_per_chunk;
+            a.list_base = p.W / 2;
+            if (e == hipSuccess)
+                e = launch_scan_rq(p, a, s);
+        } else if (p.kind == 1)
             e = launch_scan_rq(p, a, s);
         else
             e = p.dtype == 1

@@ -13,10 +13,12 @@ struct ScanArgs {
     const float *bank_norms, *qn;
     int B, N, d, k, nks, nksp, n_chunks, n_qt;
     long rows_per_chunk;
+    long row_lo, row_hi;      // query-resident scan: rows [row_lo, row_hi) of every chunk;
+    int n_lists, list_base;   // its lists: list_base + c*RS + half of n_lists per query
     uint32_t *tau;    // [B] shared bound (distance keys), lowered with atomicMin
-    int32_t *ccnt;    // [B][n_chunks] list lengths
-    uint32_t *ckey;   // [B][n_chunks][k]
-    int32_t *cidx;    // [B][n_chunks][k]
+    int32_t *ccnt;    // [B][lists] list lengths
+    uint32_t *ckey;   // [B][lists][k]
+    int32_t *cidx;    // [B][lists][k]
     uint32_t *ovf;    // per wave: [3][ovf_cap] candidates past the LDS staging area
     int ovf_cap;      // 16*RT*16*NG - STAGE_CAP (every (row, query) pair of an iteration)
 };

@@ -53,7 +53,8 @@ __device__ __forceinline__ uint32_t rq_chunk(int ri, int rg, int c)
 // all the waves. Each wave keeps, per owned query, its own list of the k
 // best candidates of its rows of the chunk (no other wave touches it) and its
 // own candidate threshold; the lists start from the shared bound the seed
-// pass computed. A chunk therefore leaves RS lists per query.
+// pass computed. A chunk therefore leaves RS lists per query (per pass, when
+// the scan takes the rows of every chunk in two launches).
 template <int NKS, int QW, int RS, int SPB, int S>
 __global__ __launch_bounds__(RQ_WAVES * WAVE, 1) void rq_scan_kernel(const ScanArgs A)
 {
@@ -93,8 +94,10 @@ __global__ __launch_bounds__(RQ_WAVES * WAVE, 1) void rq_scan_kernel(const ScanA
     const int col = lane & 15, jg = lane >> 4;
     const int k = A.k;
     const uint32_t rowb = (uint32_t)A.d * 2;
-    const long rbeg = (long)c * A.rows_per_chunk;
-    const long rend = min((long)A.N, rbeg + A.rows_per_chunk);
+    // rows [row_lo, row_hi) of chunk c
+    const long cbeg = (long)c * A.rows_per_chunk;
+    const long rbeg = cbeg + A.row_lo;
+    const long rend = min((long)A.N, cbeg + min(A.rows_per_chunk, A.row_hi));
     const int nrows = rend > rbeg ? (int)(rend - rbeg) : 0;
     const int n_blk = (nrows + RQ_ROWS - 1) / RQ_ROWS;
     const int n_stg = n_blk * SPB;
@@ -419,13 +422,12 @@ __global__ __launch_bounds__(RQ_WAVES * WAVE, 1) void rq_scan_kernel(const ScanA
         }
     }
 
-    // ---- the wave's lists -> workspace [B][n_chunks * RS][k], list c*RS + half
-    // of each query, valid entries first (no global-to-LDS load may still be
-    // in flight when the workgroup ends)
+    // ---- the wave's lists -> workspace [B][n_lists][k], list list_base +
+    // c*RS + half of each query, valid entries first (no global-to-LDS load
+    // may still be in flight when the workgroup ends)
     wait_vmcnt<0>();
     if (!active)
         return;
-    const int W = A.n_chunks * RS;
     for (int i = 0; i < QPW; ++i) {
         const int q = qw0 + i;
         if (q >= A.B)
@@ -434,7 +436,7 @@ __global__ __launch_bounds__(RQ_WAVES * WAVE, 1) void rq_scan_kernel(const ScanA
         const uint32_t key = (uint32_t)(v >> 32);
         const bool valid = key != KEY_NONE;
         const uint64_t m = ballot(valid);
-        const size_t o = (size_t)q * W + c * RS + half;
+        const size_t o = (size_t)q * A.n_lists + A.list_base + c * RS + half;
         if (valid) {
             const int pos = mbcnt(m);
             A.ckey[o * k + pos] = key;

@@ -118,6 +118,15 @@ KNN_CASES = [
     ("bf16", 64, 530000, 1024, 10), # d = 1024, (1, 2)
     ("bf16", 128, 30000, 1024, 64), # d = 1024, (1, 1), k = 64: half-block stages
     ("bf16", 100, 40, 1024, 33),    # fewer rows than chunks
+    ("bf16", 100, 60000, 1024, 20), # d = 1024, (1, 1), k = 20
+    # batches of more than 128 over a bank of more than 32 x 32,768 rows (where
+    # the seed covers less than 1/32 of it): two passes, the first eighth of
+    # every chunk, then the rest under the k-th smallest entry of the first
+    # pass's lists, each pass leaving its own lists
+    ("bf16", 160, 1101825, 384, 10),  # (4, 2); the last chunk ends inside the first pass
+    ("bf16", 300, 1100000, 384, 20),  # (4, 1), tiles one after the other
+    ("bf16", 200, 1100000, 768, 10),  # (2, 1)
+    ("bf16", 129, 1100000, 512, 32),  # (2, 1), k = 32: the smallest batch that splits
     # more than 256 bf16 requests whose rows are whole 64-element lines, k <= 10,
     # take the GEMM-structured scan: 256 x 256 macro tiles, 32x32x16 MFMAs
     ("bf16", 257, 3000, 128, 10),   # a second request tile of one request; two stages per tile
@@ -151,6 +160,7 @@ def test_knn_exact_ties_take_lower_index():
 
 @pytest.mark.parametrize("label,B,N,d,k", [
     ("query-resident scan", 200, 70000, 768, 10),
+    ("query-resident scan, two passes", 200, 1100000, 384, 10),
     ("seeded tile scan, one tile", 64, 70000, 768, 10),
     ("seeded tile scan, two tiles", 300, 66000, 256, 16),
     ("GEMM-structured scan", 300, 66000, 256, 10),
