@@ -35,10 +35,11 @@ BF16_PEAK_TFLOPS = 2500.0      # dense bf16 MFMA
 FP32_PEAK_TFLOPS = 157.3
 
 
-# Sources the scan kernel is built from: measured traffic is reported only for
-# the build whose sources it was taken with.
+# Sources the scan kernels and their plan (chunking, passes) are built from:
+# measured traffic is reported only for the build whose sources it was taken
+# with.
 SCAN_SOURCES = ["paper_2606_17949_amd/csrc/scan.hpp", "paper_2606_17949_amd/csrc/scan_rq.hpp",
-                "paper_2606_17949_amd/csrc/scan_gemm.hpp",
+                "paper_2606_17949_amd/csrc/scan_gemm.hpp", "paper_2606_17949_amd/csrc/knn.hip",
                 "paper_2606_17949_amd/csrc/knn_common.hpp",
                 "paper_2606_17949_amd/csrc/kernels.hpp", "paper_2606_17949_amd/csrc/common.hpp"]
 TRAFFIC_FILE = "profiles/scan_traffic.json"
@@ -173,7 +174,7 @@ def calibrate_copy():
     print(json.dumps({"calibrate_copy_bytes": n, "launches": 3}), flush=True)
 
 
-def _counter_means(path, kernel_sub, counter):
+def _counter_means(path, kernel_sub, counter, required=True):
     import csv
     import glob
     vals = []
@@ -183,6 +184,8 @@ def _counter_means(path, kernel_sub, counter):
                 if kernel_sub in r["Kernel_Name"] and r["Counter_Name"] == counter:
                     vals.append(float(r["Counter_Value"]))
     if not vals:
+        if not required:
+            return 0.0, 0
         raise SystemExit(f"no {counter} values for {kernel_sub} under {path}")
     return sum(vals) / len(vals), len(vals)
 
@@ -192,15 +195,22 @@ def record_traffic(pmc, workload):
     same counter's KiB for that copy). Reads PMC/copyfetch, PMC/copywrite and
     PMC/<workload>/fetch, PMC/<workload>/write; writes PMC/scan_traffic.json,
     the records already there (else the committed ones) with this workload's
-    replaced."""
+    replaced. A scan in two passes (list_bound_kernel dispatches present: the
+    counters were collected for kernels matching scan_kernel|list_bound) is
+    two scan-kernel dispatches and one list-bound dispatch."""
     copy_bytes = float(1 << 30)
     cf, _ = _counter_means(os.path.join(pmc, "copyfetch"), "copyBuffer", "FETCH_SIZE")
     cw, _ = _counter_means(os.path.join(pmc, "copywrite"), "copyBuffer", "WRITE_SIZE")
     sf, nf = _counter_means(os.path.join(pmc, workload, "fetch"), "scan_kernel", "FETCH_SIZE")
     sw, nw = _counter_means(os.path.join(pmc, workload, "write"), "scan_kernel", "WRITE_SIZE")
+    lf, nlf = _counter_means(os.path.join(pmc, workload, "fetch"), "list_bound", "FETCH_SIZE", False)
+    lw, _ = _counter_means(os.path.join(pmc, workload, "write"), "list_bound", "WRITE_SIZE", False)
+    if nlf:
+        sf, sw = 2 * sf + lf, 2 * sw + lw
     kf, kw = copy_bytes / cf, copy_bytes / cw     # bytes per counter unit
     rec = {"sources_sha256": scan_source_digest(),
            "fetch_size_kib": round(sf, 1), "write_size_kib": round(sw, 1), "dispatches": [nf, nw],
+           "passes": 2 if nlf else 1,
            "copy_fetch_kib_per_gib": round(cf, 1), "copy_write_kib_per_gib": round(cw, 1),
            "fetch_bytes": round(sf * kf), "write_bytes": round(sw * kw),
            "bytes_per_launch": round(sf * kf + sw * kw)}
