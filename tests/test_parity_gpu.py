@@ -106,6 +106,7 @@ KNN_CASES = [
                                     # 2,048 rows per compute unit)
     ("bf16", 90, 60000, 768, 20),   # (2, 2), k = 20
     ("bf16", 40, 530000, 384, 10),  # d = 384, (1, 2)
+    ("bf16", 40, 530000, 384, 64),  # d = 384, (1, 2), k = 64: a two-slot ring
     ("bf16", 40, 30000, 384, 10),   # the same batch over a small bank: the tile scan
     ("bf16", 100, 30000, 384, 20),  # d = 384, (2, 2), k = 20
     ("bf16", 256, 50000, 384, 10),  # d = 384, (4, 2)
