@@ -63,6 +63,9 @@ def test_noalloc_matches_route_batch():
         ("smaller fp32 batch", synth.CONFIGS["tiny"]),
         ("query-resident scan", synth.tiny_config(B=200, N=200_000, d=768, dtype="bf16",
                                                  clusters=1024)),
+        # more than 128 requests over more than 32 x 32,768 rows: two passes
+        ("query-resident scan in two passes",
+         synth.tiny_config(B=160, N=1_100_000, d=384, dtype="bf16", clusters=1024)),
     ]
     for label, cfg in cases:
         say(f"noalloc {label}: B={cfg.B} N={cfg.N} d={cfg.d} {cfg.dtype}, "
