@@ -112,10 +112,10 @@ def parse():
                     help="only measure the practical ceilings: a read-only pass over 4 GiB and "
                          "a library bf16 GEMM of the largebatch shape (yardsticks, not the path)")
     ap.add_argument("--clock-warm", type=float, default=1.0, metavar="SECONDS",
-                    help="untimed lookups of the first batch (k-NN and label average only, the "
-                         "instance state untouched) for this long before the warm-up batches, "
-                         "so that the timed batches run at the GPU's sustained clock, as in a "
-                         "serving loop that never idles (0: none)")
+                    help="untimed batches of the measured schedule, on a copy of the instance "
+                         "state (the timed batches carry the real one), for this long before "
+                         "the warm-up batches, so that the timed batches run at the GPU's "
+                         "sustained clock, as in a serving loop that never idles (0: none)")
     ap.add_argument("--graph", action="store_true",
                     help="sequential batches, each batch's calls (rb_route_batch, "
                          "rb_advance_state) captured beforehand in a HIP graph of its own; "
@@ -291,14 +291,16 @@ def main():
     for ev in ev_b + ev_e:      # torch creates the HIP event on first record
         ev.record(stream)
 
-    def step(t):
+    def step(t, state=None, out=None):
+        state = inst if state is None else state
+        out = assign[t] if out is None else out
         if opts is None:
-            rb.rb_route_batch(queries[t], bank, norms, cfg.k, g_qual, g_len, plens[t], inst,
-                              cfg.weights, ws=ws, assign=assign[t], stream=stream)
+            rb.rb_route_batch(queries[t], bank, norms, cfg.k, g_qual, g_len, plens[t], state,
+                              cfg.weights, ws=ws, assign=out, stream=stream)
         else:
-            rb.rb_route_batch_ex(queries[t], bank, norms, cfg.k, g_qual, g_len, plens[t], inst,
-                                 cfg.weights, opts[t], ws=ws, assign=assign[t], stream=stream)
-        rb.rb_advance_state(inst, carry_dt, stream=stream)
+            rb.rb_route_batch_ex(queries[t], bank, norms, cfg.k, g_qual, g_len, plens[t], state,
+                                 cfg.weights, opts[t], ws=ws, assign=out, stream=stream)
+        rb.rb_advance_state(state, carry_dt, stream=stream)
 
     # pipelined schedule: the first half of each lookup (seed and bank scan,
     # RB_FLAG_LISTS_ONLY) on s_knn; the second half (merge of the chunk lists
@@ -329,21 +331,29 @@ def main():
     ev_knn = [torch.cuda.Event() for _ in range(nb)]
     ev_mrg = [torch.cuda.Event() for _ in range(nb)]
 
-    def lookup(t):
-        if t >= n_ws:
-            s_knn.wait_event(ev_mrg[t - n_ws])
+    def lookup(t, ek=ev_knn, em=ev_mrg, i=None):
+        """Lookup of batch t's inputs as the i-th batch of its run (default
+        i = t); the event lists are indexed modulo their length (a ring longer
+        than the workspace ring keeps every event it waits for unrecorded
+        until that wait is enqueued)."""
+        i = t if i is None else i
+        if i >= n_ws:
+            s_knn.wait_event(em[(i - n_ws) % len(em)])
         rb.rb_knn_predict(queries[t], bank, norms, cfg.k, g_qual, g_len, lists_opts,
-                          ws=wss[t % n_ws], stream=s_knn)
-        ev_knn[t].record(s_knn)
+                          ws=wss[i % n_ws], stream=s_knn)
+        ek[i % len(ek)].record(s_knn)
 
-    def decide(t):
-        s_asg.wait_event(ev_knn[t])
+    def decide(t, ek=ev_knn, em=ev_mrg, i=None, state=None, out=None):
+        i = t if i is None else i
+        state = inst if state is None else state
+        out = assign[t] if out is None else out
+        s_asg.wait_event(ek[i % len(ek)])
         rb.rb_knn_predict(queries[t], bank, norms, cfg.k, g_qual, g_len, merge_opts,
-                          ws=wss[t % n_ws], q_hat=qh, l_hat=lh, stream=s_asg)
-        ev_mrg[t].record(s_asg)
-        rb.rb_assign_ex(qh, lh, plens[t], inst, cfg.weights, asg_opts[t],
-                        assign=assign[t], stream=s_asg, want_chosen=False)
-        rb.rb_advance_state(inst, carry_dt, stream=s_asg)
+                          ws=wss[i % n_ws], q_hat=qh, l_hat=lh, stream=s_asg)
+        em[i % len(em)].record(s_asg)
+        rb.rb_assign_ex(qh, lh, plens[t], state, cfg.weights, asg_opts[t],
+                        assign=out, stream=s_asg, want_chosen=False)
+        rb.rb_advance_state(state, carry_dt, stream=s_asg)
 
     def scan_events(j, timed):
         """Scan events j around the j-th batch's scan if it is a sampled one."""
@@ -371,28 +381,40 @@ def main():
         rb.rb_profile_scan_events(None, None)
 
     if args.clock_warm > 0:
-        # the GPU raises its clock only under sustained load (measured in the
-        # scan kernel with s_memtime against the 100 MHz counter: about
-        # 1.65-1.85 GHz after a few batches, 1.93-2.12 GHz after a few hundred)
-        qh_w = torch.empty(cfg.B, cfg.M, device=dev)
-        lh_w = torch.empty(cfg.B, cfg.M, device=dev)
+        # The GPU settles its clock to the load it runs: after a stretch of
+        # lookups alone the batches that followed ran slower than their steady
+        # state for about 50 batches (measured with every scan timed: the
+        # high-load scan from 450 to 380 us), after a stretch of the batch
+        # schedule itself at 390-400 us from the first one. So this untimed
+        # warm-up runs the schedule being measured, on a copy of the instance
+        # state (the timed batches carry the real one), cycling over the
+        # batches' inputs, as one unbroken stretch (no host synchronisation).
+        state_w = inst.clone()
+        out_w = torch.empty(cfg.B, dtype=torch.int32, device=dev)
+        ek = [torch.cuda.Event() for _ in range(2 * n_ws)]
+        em = [torch.cuda.Event() for _ in range(2 * n_ws)]
 
         def warm(n):
-            for _ in range(n):
-                rb.rb_knn_predict(queries[0], bank, norms, cfg.k, g_qual, g_len, ws=ws, q_hat=qh_w,
-                                  l_hat=lh_w, stream=stream)
+            if args.schedule == "sequential":
+                for i in range(n):
+                    step(i % nb, state_w, out_w)
+                return
+            for i in range(n):
+                lookup(i % nb, ek, em, i)
+                if i >= 1:
+                    decide((i - 1) % nb, ek, em, i - 1, state_w, out_w)
+            decide((n - 1) % nb, ek, em, n - 1, state_w, out_w)
         warm(2)
         torch.cuda.synchronize()
         t_w = time.perf_counter()
         warm(8)
         torch.cuda.synchronize()
         per = (time.perf_counter() - t_w) / 8
-        # one unbroken stretch of load (no host synchronisation inside it)
         n_w = max(1, int(args.clock_warm / per))
         t_w = time.perf_counter()
         warm(n_w)
         torch.cuda.synchronize()
-        log(f"clock warm-up: {n_w} untimed lookups in {time.perf_counter() - t_w:.2f} s")
+        log(f"clock warm-up: {n_w} untimed batches in {time.perf_counter() - t_w:.2f} s")
     run(list(range(W)))
     torch.cuda.synchronize()
     log("warm-up done")
