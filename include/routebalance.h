@@ -359,9 +359,9 @@ rb_status rb_advance_state(const rb_instances *inst, int I, float dt_seconds, vo
  * RB_FLAG_FROM_LISTS) made from the calling host thread records `begin` (a
  * hipEvent_t) on the call's stream immediately before the bank-scan kernel and
  * `end` immediately after it, so hipEventElapsedTime(begin, end) is that
- * kernel's duration. Pass NULL,
- * NULL to stop. The setting is per host thread; the events stay owned by the
- * caller. Always returns RB_OK. */
+ * kernel's duration (for a scan in two passes, the span of both scan launches
+ * and the bound between them). Pass NULL, NULL to stop. The setting is per
+ * host thread; the events stay owned by the caller. Always returns RB_OK. */
 rb_status rb_profile_scan_events(void *begin, void *end);
 
 #ifdef __cplusplus
